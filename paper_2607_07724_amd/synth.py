@@ -1,0 +1,232 @@
+"""Seeded synthetic inputs for causal GQA prefill.
+
+This module holds no step of the method.  It only draws the Q/K/V tensors
+(bf16 bit patterns, numpy ``uint16``) and the planted structures (duplicate
+blocks, needles) that both the GPU path and the reference oracle consume, so
+that both sides read byte-identical inputs.
+
+The workload shapes follow the attention shapes of the models the paper
+evaluates (Qwen2.5-7B-Instruct-1M: 28 query / 4 kv heads, d_head 128;
+Mistral-Nemo-2407: 32 / 8, d_head 128; Section 4.1) at the context lengths of
+its speed study (32K-128K, Table 3).  Real activations are not available, so
+Gaussian queries/values and block-offset or cluster-mixture keys stand in for
+them, with needle keys that imitate needle-in-a-haystack retrieval.
+
+Every random draw comes from ``numpy.random.PCG64`` seeded by
+``SeedSequence([seed, tensor, batch, head])``, so a head can be regenerated
+alone and the streams are independent of thread scheduling.
+"""
+from __future__ import annotations
+
+import dataclasses
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+BLOCK = 64
+KMEAN, QUEST = 0, 1
+_TQ, _TK, _TV, _TOFF, _TCENT, _TASSIGN, _TPLANT = 1, 2, 3, 4, 5, 6, 7
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    H: int
+    Hkv: int
+    d: int
+    N: int
+    k: int
+    q: float
+    backbone: int
+    keys: str            # "offset" or "mixture"
+    needles: int = 0
+    needle_pairs: bool = False
+    dup_pairs: bool = False
+    layers: int = 1
+    base_seed: int = 20260000
+
+    @property
+    def NB(self) -> int:
+        return self.N // BLOCK
+
+    @property
+    def T(self) -> int:
+        return self.N // BLOCK
+
+    def seed(self, layer: int = 0) -> int:
+        idx = {"C1": 1, "C2": 2, "C3": 3, "C4": 4, "C5": 5}.get(self.name.split("_")[0], 9)
+        return self.base_seed + 100 * idx + layer
+
+    def replace(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+
+# The five single-GPU workloads (attention shapes from Section 4.1; N from
+# Table 3; selector budgets and q as stated with each).
+WORKLOADS = {
+    # tiny: 4 q / 1 kv head, d 64, N 1024, k 4, q 0.25, K-mean, two planted pairs
+    "C1": Workload("C1", 1, 4, 1, 64, 1024, 4, 0.25, KMEAN, "offset", dup_pairs=True),
+    # Qwen2.5-7B-1M shape, 32K, K-mean, k 32, q 0.1, 8 needles
+    "C2": Workload("C2", 1, 28, 4, 128, 32768, 32, 0.1, KMEAN, "offset", needles=8),
+    # same shape at 64K, Quest, k 64, q 0.1, mixture keys, 8 near-tied needle pairs
+    "C3": Workload("C3", 1, 28, 4, 128, 65536, 64, 0.1, QUEST, "mixture", needles=16, needle_pairs=True),
+    # Mistral-Nemo shape, 128K, Quest, k 64, q 0.1 (also 0.05, 0.25), 32 needles
+    "C4": Workload("C4", 1, 32, 8, 128, 131072, 64, 0.1, QUEST, "mixture", needles=32),
+    # 28-layer stack at Qwen2.5-7B-1M shape, 128K, k 64, q 0.1, 32 needles / layer
+    "C5": Workload("C5", 1, 28, 4, 128, 131072, 64, 0.1, QUEST, "mixture", needles=32, layers=28),
+}
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """float32 -> bf16 bit pattern, round to nearest even (inputs are finite)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    r = ((u >> 16) & 1) + np.uint32(0x7FFF)
+    return ((u + r) >> 16).astype(np.uint16)
+
+
+def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
+    return (np.asarray(bits, np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def _rng(seed: int, tensor: int, b: int, h: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, tensor, b, h])))
+
+
+def _normal_head(seed, tensor, b, h, N, d):
+    return bf16_bits(_rng(seed, tensor, b, h).standard_normal((N, d), dtype=np.float32))
+
+
+def _key_head(w: Workload, seed, b, h):
+    N, d, NB = w.N, w.d, w.NB
+    g = _rng(seed, _TK, b, h)
+    noise = g.standard_normal((N, d), dtype=np.float32)
+    if w.keys == "offset":
+        go = _rng(seed, _TOFF, b, h)
+        off = go.standard_normal((NB, d), dtype=np.float32) * np.float32(0.5)
+        if w.dup_pairs:
+            # larger offsets for the planted blocks so they rank near the cut
+            off[1] *= np.float32(8.0)
+            off[2] *= np.float32(4.0)
+            off[3] *= np.float32(3.0)
+            off[6] *= np.float32(3.0)
+        k = noise.reshape(NB, BLOCK, d) + off[:, None, :]
+        return bf16_bits(k.reshape(N, d))
+    if w.keys == "mixture":
+        gc = _rng(seed, _TCENT, b, h)
+        centres = gc.standard_normal((64, d), dtype=np.float32)
+        ga = _rng(seed, _TASSIGN, b, h)
+        assign = ga.integers(0, 64, size=N)
+        k = centres[assign] + np.float32(0.3) * noise
+        return bf16_bits(k)
+    raise ValueError(w.keys)
+
+
+def _parallel(fn, items, threads):
+    if threads <= 1:
+        return [fn(x) for x in items]
+    with ThreadPoolExecutor(threads) as ex:
+        return list(ex.map(fn, items))
+
+
+@dataclasses.dataclass
+class Inputs:
+    w: Workload
+    layer: int
+    seed: int
+    Q: np.ndarray  # [B,H,N,d] uint16 (bf16 bits)
+    K: np.ndarray  # [B,Hkv,N,d]
+    V: np.ndarray  # [B,Hkv,N,d]
+    needles: list  # (b, h, query row i, key row j)
+    pairs: list    # (b, kv head, block a, block b, kind)
+
+
+def generate(w: Workload, layer: int = 0, threads: int = 8) -> Inputs:
+    seed = w.seed(layer)
+    B, H, Hkv, N, d = w.B, w.H, w.Hkv, w.N, w.d
+    Q = np.empty((B, H, N, d), np.uint16)
+    K = np.empty((B, Hkv, N, d), np.uint16)
+    V = np.empty((B, Hkv, N, d), np.uint16)
+
+    def do(item):
+        kind, b, h = item
+        if kind == "q":
+            Q[b, h] = _normal_head(seed, _TQ, b, h, N, d)
+        elif kind == "v":
+            V[b, h] = _normal_head(seed, _TV, b, h, N, d)
+        else:
+            K[b, h] = _key_head(w, seed, b, h)
+
+    items = [("q", b, h) for b in range(B) for h in range(H)]
+    items += [(kind, b, h) for kind in ("k", "v") for b in range(B) for h in range(Hkv)]
+    _parallel(do, items, threads)
+
+    pairs, needles = [], []
+    gp = _rng(seed, _TPLANT, 0, 0)
+    NB, G = w.NB, H // Hkv
+    if w.dup_pairs:
+        for b in range(B):
+            for kvh in range(Hkv):
+                # exact duplicate: block 4 := block 2 (an exact tie in every score)
+                K[b, kvh, 4 * BLOCK:5 * BLOCK] = K[b, kvh, 2 * BLOCK:3 * BLOCK]
+                pairs.append((b, kvh, 2, 4, "exact"))
+                # near duplicate: block 6 := block 3 with one element moved by one bf16 ulp
+                K[b, kvh, 6 * BLOCK:7 * BLOCK] = K[b, kvh, 3 * BLOCK:4 * BLOCK]
+                r, e = int(gp.integers(0, BLOCK)), int(gp.integers(0, d))
+                K[b, kvh, 6 * BLOCK + r, e] += np.uint16(1)
+                pairs.append((b, kvh, 3, 6, "ulp"))
+    n_plant = w.needles // 2 if w.needle_pairs else w.needles
+    for _ in range(n_plant):
+        b = int(gp.integers(0, B))
+        h = int(gp.integers(0, H))
+        i = int(gp.integers(N // 2, N))
+        t = i // BLOCK
+        if t < 3:
+            continue
+        blk = int(gp.integers(1, t))          # a non-forced visible block
+        j = blk * BLOCK + int(gp.integers(0, BLOCK))
+        qv = bf16_to_f32(Q[b, h, i])
+        key = np.float32(8.0) * qv / np.float32(np.linalg.norm(qv.astype(np.float64)))
+        K[b, h // G, j] = bf16_bits(key)
+        needles.append((b, h, i, j))
+        if w.needle_pairs:
+            blk2 = int(gp.integers(1, t))
+            if blk2 == blk:
+                blk2 = 1 + (blk % (t - 1))
+            j2 = blk2 * BLOCK + int(gp.integers(0, BLOCK))
+            K[b, h // G, j2] = K[b, h // G, j]
+            K[b, h // G, j2, int(gp.integers(0, d))] += np.uint16(1)
+            needles.append((b, h, i, j2))
+            pairs.append((b, h // G, blk, blk2, "needle"))
+    return Inputs(w, layer, seed, Q, K, V, needles, pairs)
+
+
+def dense_kv_idx(B: int, H: int, T: int) -> np.ndarray:
+    """kv_idx listing every causally visible block of each tile (0..t), then sentinel T."""
+    kv = np.full((B, H, T, T), T, np.int32)
+    for t in range(T):
+        kv[:, :, t, :t + 1] = np.arange(t + 1, dtype=np.int32)
+    return kv
+
+
+def random_kv_idx(seed: int, B: int, H: int, T: int, W: int, shuffle: bool = True,
+                  junk: bool = False) -> np.ndarray:
+    """Random kv_idx rows for attention tests: distinct blocks drawn from 0..t
+    (always including 0 and t), padded with the sentinel T.  ``junk`` also
+    sprinkles out-of-range entries (negative or > T) that must be ignored."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 99])))
+    kv = np.full((B, H, T, W), T, np.int32)
+    for b in range(B):
+        for h in range(H):
+            for t in range(T):
+                vis = np.arange(1, t, dtype=np.int32)
+                n = int(g.integers(0, min(W - 2, t - 1) + 1)) if t >= 2 and W > 2 else 0
+                pick = g.choice(vis, size=n, replace=False) if n else np.zeros(0, np.int32)
+                row = [0] + ([t] if t > 0 else []) + [int(x) for x in pick]
+                row = row[:W]
+                if shuffle:
+                    g.shuffle(row)
+                kv[b, h, t, :len(row)] = row
+                if junk and len(row) < W:
+                    kv[b, h, t, len(row)] = -int(g.integers(1, 5)) if g.random() < 0.5 else T + int(g.integers(1, 50))
+    return kv
