@@ -1,0 +1,187 @@
+/*
+ * ugbs.h -- uncertainty-gated block-sparse causal prefill attention on
+ * AMD Instinct MI355X (gfx950).  Plain C ABI.
+ *
+ * The method (Appendix A of the paper, steps A.1-A.10): keys are pooled into
+ * blocks of 64 tokens; every Q-tile of 64 query rows scores every causally
+ * visible block with the maximum over its rows; the sink block 0 and the
+ * tile's own block are always kept; a sorted top-2k over the remaining
+ * blocks gives both the kept list and the normalised cutoff margin sigma;
+ * sigma is averaged over heads, and the tiles whose head mean lies at or
+ * below the layer's q-quantile keep 2k blocks while every other tile keeps k
+ * (rho = 2, Section 3 step 5); attention then runs only over the kept blocks.
+ *
+ * Pipeline for one layer, four stream-ordered calls:
+ *   ugbs_block_meta   (K)                    -> meta
+ *   ugbs_score_select (Q, meta)              -> idx_sorted, sigma
+ *   ugbs_route        (sigma, idx_sorted)    -> kv_idx (may alias idx_sorted)
+ *   ugbs_attend       (Q, K, V, kv_idx)      -> O
+ * No call synchronises the device; none allocates device memory.
+ *
+ * Conventions shared by every entry point
+ *   - All tensor pointers are device pointers owned by the caller.  The
+ *     library never frees, keeps or allocates them.
+ *   - Tensors are contiguous, batch-major "BHND": Q and O are
+ *     [B, H, N, d], K and V are [B, H_kv, N, d], bf16 (raw 16-bit pattern).
+ *     Query head h reads kv head h / (H / H_kv).
+ *   - Prefill: the query rows are the key positions 0..N-1 (causal).
+ *     N_B = N / 64 key blocks, T = N / 64 Q-tiles (T == N_B).
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Every call only
+ *     enqueues work and returns; errors from the kernels themselves surface
+ *     at the caller's next synchronisation.
+ *   - Every argument is validated before anything is enqueued.  On error the
+ *     call returns a ugbs_status != UGBS_OK and enqueues nothing.
+ *     UGBS_ERR_HIP reports a failed launch (hipGetLastError).
+ *   - Inputs must be finite.  Calls on one stream may be issued from any
+ *     host thread; the library holds no per-call state.
+ */
+#ifndef UGBS_H
+#define UGBS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__) || defined(__clang__)
+#define UGBS_API __attribute__((visibility("default")))
+#else
+#define UGBS_API
+#endif
+
+#define UGBS_ABI_VERSION 1
+#define UGBS_BLOCK 64          /* BLOCK_M = BLOCK_N = 64 tokens (Section 3.1, 3.2) */
+#define UGBS_MAX_BLOCKS 2048   /* N_B <= 2048, i.e. N <= 131072 */
+#define UGBS_MAX_KV_WIDTH 4096 /* kv_width accepted by ugbs_attend; k_budget <= 2048 */
+
+typedef enum {
+  UGBS_OK = 0,
+  UGBS_ERR_NULL = 1,      /* a required pointer is NULL */
+  UGBS_ERR_SHAPE = 2,     /* batch/heads/seq_len/head_dim/block/kv_width invalid */
+  UGBS_ERR_BUDGET = 3,    /* k_budget outside [3, UGBS_MAX_KV_WIDTH / 2] */
+  UGBS_ERR_Q = 4,         /* q outside [0, 1] or NaN */
+  UGBS_ERR_BACKBONE = 5,  /* backbone not one of ugbs_backbone */
+  UGBS_ERR_ALIGN = 6,     /* a pointer is not aligned as documented */
+  UGBS_ERR_WORKSPACE = 7, /* workspace NULL or smaller than ugbs_workspace_bytes */
+  UGBS_ERR_HIP = 8,       /* a HIP launch failed */
+  UGBS_ERR_SCALE = 9      /* softmax_scale negative, NaN or infinite */
+} ugbs_status;
+
+/* Block-scoring backbone (Section 3.1).
+ * UGBS_KMEAN: mean-pooled keys, Eq. (block-score) / A.1-A.2.
+ * UGBS_QUEST: element-wise K-min/K-max bound, Eq. (quest-score). */
+typedef enum { UGBS_KMEAN = 0, UGBS_QUEST = 1 } ugbs_backbone;
+
+/* Problem description, following the paper's problem statement:
+ * Q, K, V shapes, block size, k_budget, q and the backbone.  rho is fixed
+ * at 2, so every kv_idx row has 2 * k_budget slots. */
+typedef struct ugbs_problem {
+  int32_t batch;        /* B >= 1 */
+  int32_t n_heads;      /* H >= 1, a multiple of n_kv_heads */
+  int32_t n_kv_heads;   /* H_kv >= 1 */
+  int32_t seq_len;      /* N: a positive multiple of 64, N / 64 <= UGBS_MAX_BLOCKS */
+  int32_t head_dim;     /* d: 64 or 128 */
+  int32_t block;        /* must be 64 */
+  int32_t k_budget;     /* k: 3 <= k <= UGBS_MAX_KV_WIDTH / 2; counts the forced sink and
+                           self blocks; with k >= N_B every tile keeps all visible blocks */
+  int32_t backbone;     /* ugbs_backbone */
+  double q;             /* trigger fraction, 0 <= q <= 1 */
+  float softmax_scale;  /* attention logit scale; 0 means 1/sqrt(head_dim) */
+  int32_t reserved;     /* must be 0 */
+} ugbs_problem;
+
+/* Stage 1 -- block metadata (A.1; Eq. (quest-score) for Quest).
+ *   K    : [B, H_kv, N, d] bf16, 16-byte aligned.
+ *   meta : UGBS_KMEAN: [B, H_kv, N_B, d] bf16, the mean of the block's 64
+ *          keys (exact sum, then rounded to nearest-even bf16).
+ *          UGBS_QUEST: [B, H_kv, N_B, 2, d] bf16, element-wise minimum then
+ *          element-wise maximum over the block's 64 keys.
+ *          16-byte aligned.  A zero is always written as +0. */
+UGBS_API int ugbs_block_meta(const ugbs_problem* p, const void* K, void* meta, void* stream);
+
+/* Stages 2+3 -- tile scores, forcing, sorted top-2k and sigma
+ * (A.2-A.6; Eqs. (tile-score), (sigma-def)).
+ *   For every Q-tile t and query head h, the candidate blocks are the
+ *   causally visible, non-forced ones C(t) = {1, ..., t-1}.  Their tile score
+ *   is the maximum over the 64 rows of the tile of
+ *     K-mean: q_r . kbar_b            Quest: sum_d max(q_rd kmax_bd, q_rd kmin_bd)
+ *   (no 1/sqrt(d): a positive scale changes neither the order nor sigma),
+ *   accumulated in fp32 from bf16 products.
+ *   Q          : [B, H, N, d] bf16, 16-byte aligned.
+ *   meta       : output of ugbs_block_meta for the same problem.
+ *   scores_in  : NULL, or [B, H, T, N_B] fp32 tile scores that replace the
+ *                computed ones (only entries in C(t) are read).
+ *   scores_out : NULL, or [B, H, T, N_B] fp32; receives the tile scores,
+ *                -inf outside C(t).
+ *   idx_sorted : [B, H, T, 2k] int32.  Row (t, h) is [0] (t = 0) or [0, t],
+ *                then C(t) ordered by score descending, lower block index
+ *                first on equal scores (-0 == +0), cut at 2k slots and
+ *                padded with the sentinel N_B.
+ *   sigma      : [B, H, T] fp32.  With F the forced list and m = k - |F|:
+ *                sigma = (c[m-1] - c[m]) / (c[0] - c[m]) over the sorted
+ *                candidate scores c (fp32 arithmetic), 0 when the
+ *                denominator is 0, and -1 when |C(t)| <= m (a saturated
+ *                tile: it keeps every visible block).
+ *   Q and meta are read-only; idx_sorted/sigma/scores_out are fully written. */
+UGBS_API int ugbs_score_select(const ugbs_problem* p, const void* Q, const void* meta,
+                      const float* scores_in, float* scores_out,
+                      int32_t* idx_sorted, float* sigma, void* stream);
+
+/* Stage 4 -- head mean, per-layer quantile trigger and padded expansion
+ * (A.7-A.9; Eq. (trigger)).
+ *   The quantile population P of a sequence is the set of tiles with more
+ *   candidates than kept slots (|C(t)| > k - |F(t)|; it depends only on N
+ *   and k).  For t in P, sigma_bar[t] = (sum over h = 0..H-1 of sigma[t,h],
+ *   fp32, in head order) / H.  With n = |P| and n_trig = ceil(q n) (computed
+ *   in double on the host), tau is the n_trig-th smallest sigma_bar over P,
+ *   and tile t triggers iff t in P and sigma_bar[t] <= tau (ties at tau all
+ *   trigger).  kv_idx = idx_sorted, with slots k..2k-1 of every row of a
+ *   tile that does not trigger overwritten by the sentinel N_B.
+ *   sigma      : [B, H, T] fp32 from ugbs_score_select.
+ *   idx_sorted : [B, H, T, 2k] int32.
+ *   kv_idx     : [B, H, T, 2k] int32; may equal idx_sorted (in place: only
+ *                the sentinel slots are written).
+ *   sigma_bar  : NULL or [B, T] fp32 (-1 outside P).
+ *   tau        : NULL or [B] fp32 (-1 when no tile triggers).
+ *   trigger    : NULL or [B, T] uint8 (0/1).
+ *   workspace  : device memory of at least ugbs_workspace_bytes(p) bytes,
+ *                256-byte aligned, owned by the caller; its contents on entry
+ *                are ignored.  Two calls that overlap in time must not share
+ *                a workspace. */
+UGBS_API int ugbs_route(const ugbs_problem* p, const float* sigma, const int32_t* idx_sorted,
+               int32_t* kv_idx, float* sigma_bar, float* tau, uint8_t* trigger,
+               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Stage 5 -- block-sparse causal attention over kv_idx (A.10; Eq. (Attn)).
+ *   For row i of tile t and query head h, the attended keys are
+ *   J_i = { j <= i : block(j) is listed in kv_idx[b, h, t, :] } and
+ *   O_i = sum_{j in J_i} softmax_j(scale * q_i . k_j) v_j, computed with bf16
+ *   products, fp32 accumulation and an fp32 online softmax.  Entries outside
+ *   [0, N_B) (the sentinel N_B included) and blocks after t are skipped.
+ *   Entries of a row must be distinct (a repeated block is undefined, but
+ *   is never read out of bounds).  A row with no attended key gives O = 0.
+ *   kv_idx with every block 0..t listed (kv_width = N_B) is dense causal
+ *   attention.
+ *   Q, K, V : as in the conventions above, 16-byte aligned.
+ *   kv_idx  : [B, H, T, kv_width] int32, 4-byte aligned.
+ *   kv_width: 1 <= kv_width <= UGBS_MAX_KV_WIDTH (2k for the pipeline).
+ *   O       : [B, H, N, d] bf16, 16-byte aligned; fully written. */
+UGBS_API int ugbs_attend(const ugbs_problem* p, const void* Q, const void* K, const void* V,
+                const int32_t* kv_idx, int32_t kv_width, void* O, void* stream);
+
+/* Bytes of device workspace ugbs_route needs for problem p (0 if p is invalid). */
+UGBS_API size_t ugbs_workspace_bytes(const ugbs_problem* p);
+
+/* Static, human-readable text for a ugbs_status value. */
+UGBS_API const char* ugbs_status_string(int status);
+
+/* UGBS_ABI_VERSION of the loaded library. */
+UGBS_API int ugbs_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UGBS_H */

@@ -1,0 +1,74 @@
+// Internal declarations shared by the HIP translation units of libugbs.
+// Device helpers here are the GPU path's own; nothing is shared with the
+// reference oracle.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ugbs.h"
+
+namespace ugbs {
+
+constexpr int kBlock = UGBS_BLOCK;
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+// Validated problem with derived sizes; passed by value to launchers.
+struct Shape {
+  int B, H, Hkv, G, N, d, NB, T, k, W, backbone;
+  double q;
+  float scale;
+};
+
+// Launchers (each enqueues on `stream` and returns hipGetLastError()).
+hipError_t launch_block_meta(const Shape& s, const uint16_t* K, uint16_t* meta,
+                             hipStream_t stream);
+hipError_t launch_score_select(const Shape& s, const uint16_t* Q, const uint16_t* meta,
+                               const float* scores_in, float* scores_out,
+                               int32_t* idx_sorted, float* sigma, hipStream_t stream);
+hipError_t launch_route(const Shape& s, int n_pop, int n_trig, const float* sigma,
+                        const int32_t* idx_sorted, int32_t* kv_idx, float* sigma_bar,
+                        float* tau, uint8_t* trigger, void* workspace, hipStream_t stream);
+hipError_t launch_attend(const Shape& s, const uint16_t* Q, const uint16_t* K,
+                         const uint16_t* V, const int32_t* kv_idx, int kv_width,
+                         uint16_t* O, hipStream_t stream);
+
+// Route workspace layout: sigma_bar [B*T] f32 | tau [B] f32 | trigger [B*T] u8.
+inline size_t ws_align(size_t x) { return (x + 255) & ~size_t(255); }
+inline size_t ws_sigma_bar_off(const Shape&) { return 0; }
+inline size_t ws_tau_off(const Shape& s) { return ws_align(sizeof(float) * size_t(s.B) * s.T); }
+inline size_t ws_trigger_off(const Shape& s) {
+  return ws_tau_off(s) + ws_align(sizeof(float) * size_t(s.B));
+}
+inline size_t ws_total(const Shape& s) { return ws_trigger_off(s) + ws_align(size_t(s.B) * s.T); }
+
+// Work-unit ordering used by the per-(tile, head) kernels: consecutive
+// workgroup ids are dealt round-robin to the 8 XCDs, so the id is remapped
+// to give each XCD a contiguous range of units.  Within the range, units go
+// kv head by kv head (its metadata and K/V stay in that XCD's L2), heaviest
+// tile first (work grows with t), sibling query heads adjacent.
+struct Unit {
+  int b, h, t;
+};
+
+__device__ __forceinline__ int xcd_remap(int id, int n_total) {
+  const int per = (n_total + 7) / 8;
+  return (id % 8) * per + id / 8;
+}
+
+__device__ __forceinline__ Unit unit_of(int u, const Shape& s) {
+  Unit r;
+  const int g = u % s.G;
+  int rest = u / s.G;
+  const int tr = rest % s.T;
+  rest /= s.T;
+  const int kvh = rest % s.Hkv;
+  r.b = rest / s.Hkv;
+  r.t = s.T - 1 - tr;
+  r.h = kvh * s.G + g;
+  return r;
+}
+
+}  // namespace ugbs
