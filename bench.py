@@ -1,0 +1,306 @@
+"""Benchmark: routed block-sparse causal prefill on one MI355X.
+
+One step = one pass of the whole pipeline for one layer (block metadata ->
+tile scores + top-2k + sigma -> quantile route -> sparse attention) over one
+batch of synthetic input already resident in HBM.  Default workload: the
+Mistral-Nemo attention shape (32 query / 8 kv heads, d 128) at N = 131072,
+Quest backbone, k 64, q 0.1 (Table 3 context length; Section 4.1 shapes).
+
+Printed (one JSON line): pipeline time and effective TFLOP/s, per-stage
+times, the same-run dense causal attention (torch SDPA and this library's
+kernel with every block listed), the roofline figures of the dominant
+kernel (timed live with HIP events on its stream), and the reference oracle
+timed on the host cores over a bounded sample of the same workload.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "routed block-sparse prefill ms + TFLOP/s vs dense at 32K-128K, 1 MI355X"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="C4", choices=["C2", "C3", "C4"])
+    ap.add_argument("--q", type=float, default=None)
+    ap.add_argument("--cpu-units", type=int, default=3072, help="oracle sample size (tile, head units)")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--json-out", default=None)
+    return ap.parse_args()
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def flops_attention(kv_idx: np.ndarray, NB: int, d: int) -> float:
+    """4 d per attended (query, key) pair; exact causal pair count per unit."""
+    T = kv_idx.shape[2]
+    t = np.arange(T)[None, None, :, None]
+    valid = (kv_idx >= 0) & (kv_idx <= t)
+    diag = (kv_idx == t) & valid
+    full = valid & ~diag
+    pairs = full.sum(dtype=np.int64) * 64 * 64 + diag.sum(dtype=np.int64) * (64 * 65 // 2)
+    return 4.0 * d * float(pairs)
+
+
+def flops_scores(B: int, H: int, T: int, d: int, backbone: int) -> float:
+    """2 * KD per (row, candidate block): KD = d (K-mean) or 2d (Quest split form)."""
+    KD = d * (2 if backbone == 1 else 1)
+    cand = sum(max(t - 1, 0) for t in range(T))
+    return 2.0 * KD * B * H * 64 * cand
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (asked for --gpus {a.gpus}); the method's "
+              "multi-GPU sharding is described in DESIGN.md but not built", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2607_07724_amd as ugbs
+    from paper_2607_07724_amd import synth
+
+    w = synth.WORKLOADS[a.workload]
+    if a.q is not None:
+        w = w.replace(q=a.q)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"workload {w.name}: B={w.B} H={w.H}/{w.Hkv} d={w.d} N={w.N} k={w.k} q={w.q} backbone={w.backbone}")
+    t0 = time.time()
+    inp = synth.generate(w, threads=16)
+    log(f"inputs generated in {time.time() - t0:.1f}s")
+
+    def to_dev(x):
+        return torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+
+    Q, K, V = to_dev(inp.Q), to_dev(inp.K), to_dev(inp.V)
+    p = ugbs.Problem.make(w.B, w.H, w.Hkv, w.N, w.d, w.k, w.q, w.backbone)
+    bufs = ugbs.Buffers(p, device=dev)
+    O = torch.empty_like(Q)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        ugbs.ugbs_block_meta(p, K, bufs.meta)
+        if ev is not None:
+            ev[1].record(stream)
+        ugbs.ugbs_score_select(p, Q, bufs.meta, bufs.idx_sorted, bufs.sigma)
+        if ev is not None:
+            ev[2].record(stream)
+        ugbs.ugbs_route(p, bufs.sigma, bufs.idx_sorted, bufs.kv_idx, bufs.workspace,
+                        bufs.sigma_bar, bufs.tau, bufs.trigger)
+        if ev is not None:
+            ev[3].record(stream)
+        ugbs.ugbs_attend(p, Q, K, V, bufs.kv_idx, O)
+        if ev is not None:
+            ev[4].record(stream)
+
+    for i in range(a.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+    log(f"warmup done ({a.warmup} steps)")
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(a.steps)]
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for i in range(a.steps):
+        step(evs[i])
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t0
+    ms_per_step = 1e3 * wall / a.steps
+    stage_ms = np.array([[evs[i][j].elapsed_time(evs[i][j + 1]) for j in range(4)] for i in range(a.steps)])
+    stage_avg = stage_ms.mean(axis=0)
+    log(f"timed {a.steps} steps: {ms_per_step:.3f} ms/step; stages {np.round(stage_avg, 4).tolist()}")
+
+    kv = bufs.kv_idx.cpu().numpy()
+    trig = bufs.trigger.cpu().numpy()
+    f_att = flops_attention(kv, w.NB, w.d)
+    f_sc = flops_scores(w.B, w.H, w.T, w.d, w.backbone)
+    f_dense = 4.0 * w.d * w.B * w.H * (w.N * (w.N + 1) / 2)
+    kept = (kv != w.NB).sum(axis=-1)
+    # needle hit rate: the needle's block kept in its query's tile row
+    hits = [int(np.any(kv[b, h, i // 64] == j // 64)) for (b, h, i, j) in inp.needles]
+    hit_rate = float(np.mean(hits)) if hits else None
+
+    att_ms = float(stage_avg[3])
+    bytes_kv_gathered = 2.0 * float(kept.sum()) * 64 * w.d * 2
+    roofline = {
+        "kernel": "attend_kernel<128>",
+        "bound": "mfma",
+        "achieved": round(f_att / (att_ms * 1e-3) / 1e12, 2),
+        "peak": PEAK_BF16_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": round(f_att / (att_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "traffic": None,
+        "flop_per_launch": f_att,
+        "gathered_kv_bytes_per_launch": bytes_kv_gathered,
+        "gathered_kv_GBps": round(bytes_kv_gathered / (att_ms * 1e-3) / 1e9, 1),
+    }
+    meta_bytes = w.B * w.Hkv * w.N * w.d * 2 + w.B * w.Hkv * w.NB * w.d * 2 * (2 if w.backbone == 1 else 1)
+    stages = {
+        "block_meta": {"ms": round(float(stage_avg[0]), 4),
+                       "GBps": round(meta_bytes / (stage_avg[0] * 1e-3) / 1e9, 1)},
+        "score_select": {"ms": round(float(stage_avg[1]), 4),
+                         "TFLOPs": round(f_sc / (stage_avg[1] * 1e-3) / 1e12, 2),
+                         "Q_GBps": round(w.B * w.H * w.N * w.d * 2 / (stage_avg[1] * 1e-3) / 1e9, 1)},
+        "route": {"ms": round(float(stage_avg[2]), 4)},
+        "attend": {"ms": round(att_ms, 4), "TFLOPs": roofline["achieved"]},
+    }
+
+    dense = None
+    if not a.no_dense:
+        import torch.nn.functional as F
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        # torch SDPA (the paper's dense kind), GQA heads shared
+        sd_ms = None
+        try:
+            from torch.nn.attention import SDPBackend, sdpa_kernel
+            G = w.H // w.Hkv
+            Ke, Ve = K.repeat_interleave(G, dim=1), V.repeat_interleave(G, dim=1)
+            with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
+                F.scaled_dot_product_attention(Q, Ke, Ve, is_causal=True)
+                torch.cuda.synchronize(dev)
+                reps = 3
+                e0.record(stream)
+                for _ in range(reps):
+                    F.scaled_dot_product_attention(Q, Ke, Ve, is_causal=True)
+                e1.record(stream)
+                torch.cuda.synchronize(dev)
+            sd_ms = e0.elapsed_time(e1) / reps
+            del Ke, Ve
+        except Exception as ex:  # keep the routed figures even if SDPA is unavailable
+            log(f"torch SDPA failed: {ex!r}")
+        # this library's attention kernel with every causal block listed
+        kvd = torch.from_numpy(synth.dense_kv_idx(w.B, w.H, w.T)).to(dev)
+        pd = ugbs.Problem.make(w.B, w.H, w.Hkv, w.N, w.d, w.NB, 0.0, w.backbone)
+        Od = torch.empty_like(Q)
+        ugbs.ugbs_attend(pd, Q, K, V, kvd, Od)
+        torch.cuda.synchronize(dev)
+        reps = 2
+        e0.record(stream)
+        for _ in range(reps):
+            ugbs.ugbs_attend(pd, Q, K, V, kvd, Od)
+        e1.record(stream)
+        torch.cuda.synchronize(dev)
+        ud_ms = e0.elapsed_time(e1) / reps
+        del kvd, Od
+        dense = {
+            "torch_sdpa_ms": None if sd_ms is None else round(sd_ms, 3),
+            "torch_sdpa_TFLOPs": None if sd_ms is None else round(f_dense / (sd_ms * 1e-3) / 1e12, 1),
+            "ugbs_attend_dense_ms": round(ud_ms, 3),
+            "ugbs_attend_dense_TFLOPs": round(f_dense / (ud_ms * 1e-3) / 1e12, 1),
+            "routed_over_sdpa": None if sd_ms is None else round(ms_per_step / sd_ms, 4),
+            "dense_flop": f_dense,
+        }
+        log(f"dense: {dense}")
+
+    cpu = None
+    if not a.no_cpu:
+        cpu = cpu_baseline(w, inp, a.cpu_units)
+        log(f"cpu baseline: {cpu}")
+
+    value = (f_sc + f_att) / (ms_per_step * 1e-3) / 1e12
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{w.name}: Mistral-Nemo-shaped causal GQA prefill layer" if w.name == "C4" else w.name,
+            "batch": w.B, "q_heads": w.H, "kv_heads": w.Hkv, "head_dim": w.d, "seq_len": w.N,
+            "block": 64, "k_budget": w.k, "q": w.q, "rho": 2,
+            "backbone": "quest" if w.backbone == 1 else "kmean", "seed": w.seed(0),
+        },
+        "flop": {"score": f_sc, "attention": f_att, "dense_equivalent_TFLOPs":
+                 round(f_dense / (ms_per_step * 1e-3) / 1e12, 1)},
+        "stages": stages,
+        "dense": dense,
+        "selection": {"mean_kept_blocks": round(float(kept.mean()), 3),
+                      "triggered_tiles": int(trig.sum()),
+                      "needle_hit_rate": hit_rate},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    line = json.dumps(out)
+    print(line, flush=True)
+    if a.json_out:
+        with open(a.json_out, "w") as f:
+            f.write(line + "\n")
+
+
+def cpu_baseline(w, inp, n_units):
+    """The reference oracle on a bounded sample of the same workload: block
+    metadata for every kv head, then tile scores, top-2k/sigma and exact
+    attention (over the oracle's own kept list) for `n_units` random
+    (tile, head) units; throughput in the metric's unit."""
+    import oracle
+    threads = min(os.cpu_count() or 1, 16)
+    g = np.random.default_rng(w.seed(0))
+    units = np.stack([np.zeros(n_units, np.int32),
+                      g.integers(0, w.H, n_units).astype(np.int32),
+                      g.integers(w.k, w.T, n_units).astype(np.int32)], axis=1)
+    t0 = time.perf_counter()
+    meta = oracle.block_meta(w.backbone, inp.K, nthreads=threads)
+    t1 = time.perf_counter()
+    S = oracle.tile_scores(w.backbone, inp.Q, meta, w.Hkv, units=units, nthreads=threads)
+    idx, sig = oracle.select(S, w.k, t_of_row=units[:, 2])
+    t2 = time.perf_counter()
+    oracle.attend(inp.Q, inp.K, inp.V, kv_idx=idx, units=units, nthreads=threads)
+    t3 = time.perf_counter()
+    KD = w.d * (2 if w.backbone == 1 else 1)
+    f_sc = float(sum(2 * KD * 64 * max(int(t) - 1, 0) for t in units[:, 2]))
+    # every sampled row lists its own (diagonal) block plus n - 1 earlier ones
+    f_at = float(sum(4 * w.d * (64 * 64 * (int((r != w.NB).sum()) - 1) + 64 * 65 // 2) for r in idx))
+    secs = t3 - t0
+    return {
+        "value": round((f_sc + f_at) / secs / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "seconds": round(secs, 2),
+        "seconds_meta_scores_attend": [round(t1 - t0, 2), round(t2 - t1, 2), round(t3 - t2, 2)],
+        "sample": f"block metadata for all {w.B * w.Hkv} kv heads, then scores+top-2k+sigma and "
+                  f"exact fp64 attention for {n_units} random (tile>=k, head) units of the same "
+                  f"{w.name} inputs; route skipped (needs every tile)",
+        "host_cpu": _cpu_name(),
+    }
+
+
+def _cpu_name():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+if __name__ == "__main__":
+    main()
