@@ -3,23 +3,38 @@
 // One workgroup of two waves per (batch, query head, Q-tile) unit; wave w
 // owns query rows 32w..32w+31 of the tile.  The tile's kv_idx row is first
 // compacted into LDS (entries outside 0..t are dropped, order kept), then
-// the listed key blocks are visited one by one:
-//   - the next block's K and V are fetched into registers while the current
-//     block is computed, then written to LDS: K as [key][d], V transposed as
-//     [d][key] (both rows padded by 16 bytes against bank conflicts);
-//   - S^T = K Q^T on v_mfma_f32_16x16x32_bf16 (K from LDS is the A operand,
-//     the wave's 32 query rows stay in registers as the B operand), so each
-//     lane holds the scores of one query row for 16 keys;
-//   - fp32 online softmax in base 2 (the log2(e) factor is folded into the
-//     scale); only the diagonal block t is masked (key > row);
-//   - O^T += V^T P^T on the same MFMA: the lane's probabilities, packed to
-//     bf16, are already the B operand, and V^T rows from LDS are the A
-//     operand.
+// the listed key blocks are visited one by one.
+//
+// Staging.  K and V blocks (64 keys x d, bf16) go global -> LDS with
+// direct-to-LDS loads (global_load_lds_dwordx4: no registers, no VALU).
+// Both live unpadded in natural [key][d] layout with the 16-byte column c of
+// row r stored at column c ^ (r mod d/8), which makes the MFMA operand reads
+// below bank-conflict free or nearly so.  K and V have one buffer each and
+// are refilled in a split ping-pong: K(i+1) is fetched as soon as both waves
+// have finished S(i), V(i+1) as soon as both have finished PV(i), so the
+// fetches overlap the softmax and the other matrix product.
+//
+// Compute, per block and wave (v_mfma_f32_16x16x32_bf16):
+//   S^T = K Q^T   K rows from LDS (ds_read_b128) are the A operand; the
+//                 wave's 32 query rows stay in registers as the B operand;
+//                 each lane ends up holding 16 keys of one query row.
+//   softmax       fp32 online softmax in base 2 (log2 e folded into the
+//                 scale); only the diagonal block t is masked (key > row);
+//                 the O rescale is skipped when no row max moved.
+//   O^T += V^T P^T  the lane's probabilities, packed to bf16, already are
+//                 the B operand; V^T comes straight from the natural-layout
+//                 LDS tile through the transposing read ds_read_b64_tr_b16
+//                 (16 lanes fetch a 4-key x 16-channel patch and each lane
+//                 receives the 4 keys of one channel).
 // Per listed block and unit: 4*64*64*d FLOP on 2*64*d*2 bytes of K/V.
 #include "ugbs_internal.h"
 
 namespace ugbs {
 namespace {
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+#define LDS_AS __attribute__((address_space(3)))
+#define GLB_AS __attribute__((address_space(1)))
 
 struct AttnParams {
   Shape s;
@@ -40,26 +55,74 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
   return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
 }
 
-template <int D>
-struct Smem {
-  static constexpr int kStride = D + 8;      // K row stride (bf16)
-  static constexpr int vStride = kBlock + 8; // V^T row stride (bf16)
-  static constexpr int kBytes = kBlock * kStride * 2;
-  static constexpr int vBytes = D * vStride * 2;
-  static constexpr int listOff = kBytes + vBytes;
-};
+// s_waitcnt immediates (gfx9 encoding): vmcnt in bits 3:0 and 15:14,
+// expcnt 6:4, lgkmcnt 11:8.  Other counters are left at "no wait".
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | 0x70 | 0xf00);
+}
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xc07f); }
+
+// Workgroup barrier for LDS hand-offs only: no memory fence, so in-flight
+// direct-to-LDS prefetches are not drained.  Callers wait on the counters
+// they need first.  The empty asm keeps the compiler from moving memory
+// operations across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 template <int D>
-__global__ void __launch_bounds__(128) attend_kernel(AttnParams P) {
-  using L = Smem<D>;
+struct Tile {
+  static constexpr int CPR = D / 8;                 // 16-byte chunks per key row
+  static constexpr int kElems = kBlock * D;         // one K or V block
+  static constexpr int kLoads = kBlock * CPR / 64;  // direct loads per block (64 chunks each)
+  static constexpr int kLoadsPerWave = kLoads / 2;
+  // element offset of 16-byte column c of row r in the swizzled tile
+  __device__ static __forceinline__ int off(int r, int c) { return (r * CPR + (c ^ (r & (CPR - 1)))) * 8; }
+};
+
+// One direct-to-LDS 16-byte load per lane: M0 holds the wave-uniform LDS
+// destination, lane l's data lands at M0 + 16 l.  Issued from inline asm so
+// the compiler's wait-count insertion does not drain it before unrelated LDS
+// reads; the kernel waits on vmcnt explicitly (no other vector memory
+// operation is in flight while these are).
+__device__ __forceinline__ void dma16(const uint16_t* src, uint32_t lds_byte_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(lds_byte_addr)
+               : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const LDS_AS void*)p;
+}
+
+template <int D>
+__device__ __forceinline__ void fetch_block(const uint16_t* src_blk, uint16_t* tile, int w, int lane) {
+  using L = Tile<D>;
+  const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr(tile));
+#pragma unroll
+  for (int i = 0; i < L::kLoadsPerWave; ++i) {
+    const int inst = w * L::kLoadsPerWave + i;
+    const int p = inst * 64 + lane;                 // LDS chunk written by this lane
+    const int r = p / L::CPR;
+    const int c = (p % L::CPR) ^ (r & (L::CPR - 1));  // global chunk that belongs there
+    dma16(src_blk + r * D + c * 8, __builtin_amdgcn_readfirstlane(base + inst * 64 * 16));
+  }
+}
+
+template <int D>
+__global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) attend_kernel(AttnParams P) {
+  using L = Tile<D>;
   constexpr int KS = D / 32;      // k-steps of QK^T
-  constexpr int DT = D / 16;      // 16-wide d tiles of O^T
-  constexpr int KCH = kBlock * D / 8 / 128;  // 16-byte K chunks per thread
-  constexpr int VP = D / 64;      // V passes (8 d-groups of 8 channels each)
-  extern __shared__ __align__(16) unsigned char smem[];
-  uint16_t* s_k = reinterpret_cast<uint16_t*>(smem);
-  uint16_t* s_vt = reinterpret_cast<uint16_t*>(smem + L::kBytes);
-  int32_t* s_list = reinterpret_cast<int32_t*>(smem + L::listOff);
+  constexpr int DT = D / 16;      // 16-channel tiles of O^T
+  constexpr int NW = L::kLoadsPerWave;
+  __shared__ __align__(16) uint16_t s_k[L::kElems];
+  __shared__ __align__(16) uint16_t s_v[L::kElems];
+  extern __shared__ int32_t s_list[];
   __shared__ int s_n;
 
   const Shape& s = P.s;
@@ -104,49 +167,13 @@ __global__ void __launch_bounds__(128) attend_kernel(AttnParams P) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) bq[rt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qr + 32 * ks));
   }
+  wait_vmcnt<0>();
 
   const uint16_t* Kh = P.K + ((size_t)u.b * s.Hkv + kvh) * s.N * D;
   const uint16_t* Vh = P.V + ((size_t)u.b * s.Hkv + kvh) * s.N * D;
-
-  uint4 rk[KCH];
-  uint4 rv[VP][4];
-  const int vkg = tid & 15, vdg = tid >> 4;  // V: keys 4*vkg..+3, channels 8*vdg..+7 (+64 per pass)
-  auto fetch = [&](int blk) {
-    const uint16_t* kb = Kh + (size_t)blk * kBlock * D;
-#pragma unroll
-    for (int j = 0; j < KCH; ++j) {
-      const int c = tid + 128 * j;
-      rk[j] = *reinterpret_cast<const uint4*>(kb + (size_t)(c / (D / 8)) * D + (c % (D / 8)) * 8);
-    }
-    const uint16_t* vb = Vh + (size_t)blk * kBlock * D;
-#pragma unroll
-    for (int pv = 0; pv < VP; ++pv)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        rv[pv][r] = *reinterpret_cast<const uint4*>(vb + (size_t)(4 * vkg + r) * D + 64 * pv + 8 * vdg);
-  };
-  auto stash = [&]() {
-#pragma unroll
-    for (int j = 0; j < KCH; ++j) {
-      const int c = tid + 128 * j;
-      *reinterpret_cast<uint4*>(s_k + (c / (D / 8)) * L::kStride + (c % (D / 8)) * 8) = rk[j];
-    }
-#pragma unroll
-    for (int pv = 0; pv < VP; ++pv) {
-      const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&rv[pv][0]);
-      const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&rv[pv][1]);
-      const uint32_t* r2 = reinterpret_cast<const uint32_t*>(&rv[pv][2]);
-      const uint32_t* r3 = reinterpret_cast<const uint32_t*>(&rv[pv][3]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int wd = e >> 1, sh = (e & 1) * 16;
-        const uint32_t x0 = (r0[wd] >> sh) & 0xffffu, x1 = (r1[wd] >> sh) & 0xffffu;
-        const uint32_t x2 = (r2[wd] >> sh) & 0xffffu, x3 = (r3[wd] >> sh) & 0xffffu;
-        uint2 pk = make_uint2(x0 | (x1 << 16), x2 | (x3 << 16));
-        *reinterpret_cast<uint2*>(s_vt + (64 * pv + 8 * vdg + e) * L::vStride + 4 * vkg) = pk;
-      }
-    }
-  };
+  int blk = s_list[0];
+  fetch_block<D>(Kh + (size_t)blk * Tile<D>::kElems, s_k, w, lane);
+  fetch_block<D>(Vh + (size_t)blk * Tile<D>::kElems, s_v, w, lane);
 
   f32x4 acc_o[DT][2];
 #pragma unroll
@@ -156,13 +183,13 @@ __global__ void __launch_bounds__(128) attend_kernel(AttnParams P) {
   float m_run[2] = {-__builtin_huge_valf(), -__builtin_huge_valf()};
   float l_run[2] = {0.f, 0.f};
 
-  fetch(s_list[0]);
-  stash();
-  __syncthreads();
-
   for (int it = 0; it < n; ++it) {
-    const int blk = s_list[it];
-    if (it + 1 < n) fetch(s_list[it + 1]);
+    const bool has_next = it + 1 < n;
+    const int nblk = has_next ? s_list[it + 1] : 0;
+
+    // K(it) landed (V(it) may still be in flight)
+    wait_vmcnt<NW>();
+    lds_barrier();
 
     // S^T = K Q^T : [64 keys x 32 rows] per wave
     f32x4 sc[4][2];
@@ -174,18 +201,22 @@ __global__ void __launch_bounds__(128) attend_kernel(AttnParams P) {
     for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
-        const bf16x8 ak = as_bf16x8(*reinterpret_cast<const uint4*>(
-            s_k + (16 * kt + c16) * L::kStride + 32 * ks + 8 * g));
+        const int r = 16 * kt + c16;
+        const bf16x8 ak = as_bf16x8(*reinterpret_cast<const uint4*>(s_k + L::off(r, 4 * ks + g)));
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
           sc[kt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, bq[rt][ks], sc[kt][rt], 0, 0, 0);
       }
     }
+    wait_lgkm0();
+    lds_barrier();                       // both waves are done reading s_k
+    if (has_next) fetch_block<D>(Kh + (size_t)nblk * Tile<D>::kElems, s_k, w, lane);
 
     // online softmax (base 2); lane holds row (32w + 16rt + c16), keys 16kt + 4g + i
     const bool diag = (blk == u.t);
     float alpha[2];
     uint32_t pb[2][2][4];
+    bool moved = false;
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
       const int r = 32 * w + 16 * rt + c16;
@@ -194,15 +225,14 @@ __global__ void __launch_bounds__(128) attend_kernel(AttnParams P) {
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float v = sc[kt][rt][i] * P.scale_log2;
-          if (diag && (16 * kt + 4 * g + i) > r) v = -__builtin_huge_valf();
-          sc[kt][rt][i] = v;
-          mx = fmaxf(mx, v);
+          if (diag && (16 * kt + 4 * g + i) > r) sc[kt][rt][i] = -__builtin_huge_valf();
+          mx = fmaxf(mx, sc[kt][rt][i]);
         }
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run[rt], mx);
-      alpha[rt] = exp2f(m_run[rt] - m_new);
+      const float m_new = fmaxf(m_run[rt], mx * P.scale_log2);
+      moved |= m_new != m_run[rt];
+      alpha[rt] = __builtin_amdgcn_exp2f(m_run[rt] - m_new);
       m_run[rt] = m_new;
       float ls = 0.f;
       float p[4][4];
@@ -210,7 +240,7 @@ __global__ void __launch_bounds__(128) attend_kernel(AttnParams P) {
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          p[kt][i] = exp2f(sc[kt][rt][i] - m_new);
+          p[kt][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[kt][rt][i], P.scale_log2, -m_new));
           ls += p[kt][i];
         }
       l_run[rt] = l_run[rt] * alpha[rt] + ls;
@@ -222,22 +252,35 @@ __global__ void __launch_bounds__(128) attend_kernel(AttnParams P) {
         pb[rt][j][3] = pack_bf16(p[2 * j + 1][2], p[2 * j + 1][3]);
       }
     }
+    if (__ballot(moved)) {
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
+      for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
+        for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc_o[dt][rt][i] *= alpha[rt];
+          for (int i = 0; i < 4; ++i) acc_o[dt][rt][i] *= alpha[rt];
+    }
 
-    // O^T += V^T P^T
+    // V(it) landed (K(it+1) may still be in flight)
+    if (has_next) wait_vmcnt<NW>(); else wait_vmcnt<0>();
+    lds_barrier();
+
+    // O^T += V^T P^T ; lane (channel 16dt + c16, group g) takes keys
+    // 32j + 4g + 0..3 and 32j + 16 + 4g + 0..3 through two transposing reads
+    const int tr_row = 4 * g + (c16 >> 2);
+    const int tr_col = (c16 & 3) >> 1, tr_half = (c16 & 1) * 4;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const uint16_t* vr = s_vt + (16 * dt + c16) * L::vStride + 32 * j + 4 * g;
-        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
-        const bf16x8 av = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+        const int r0 = 32 * j + tr_row, r1 = r0 + 16;
+        const int c = 2 * dt + tr_col;
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (LDS_AS v4i16*)(s_v + L::off(r0, c) + tr_half));
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (LDS_AS v4i16*)(s_v + L::off(r1, c) + tr_half));
+        const bf16x8 av = __builtin_bit_cast(
+            bf16x8, (short __attribute__((ext_vector_type(8)))){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
           const bf16x8 bp = as_bf16x8(make_uint4(pb[rt][j][0], pb[rt][j][1], pb[rt][j][2], pb[rt][j][3]));
@@ -245,12 +288,10 @@ __global__ void __launch_bounds__(128) attend_kernel(AttnParams P) {
         }
       }
     }
-
-    __syncthreads();
-    if (it + 1 < n) {
-      stash();
-      __syncthreads();
-    }
+    wait_lgkm0();
+    lds_barrier();                       // both waves are done reading s_v
+    if (has_next) fetch_block<D>(Vh + (size_t)nblk * Tile<D>::kElems, s_v, w, lane);
+    blk = nblk;
   }
 
   // ---- normalise and store: lane holds O^T[16dt + 4g + i][row] ------------
@@ -273,8 +314,7 @@ __global__ void __launch_bounds__(128) attend_kernel(AttnParams P) {
 
 template <int D>
 hipError_t launch_t(const AttnParams& P, hipStream_t stream) {
-  using L = Smem<D>;
-  const size_t smem = L::listOff + sizeof(int32_t) * (size_t)P.kv_width;
+  const size_t smem = sizeof(int32_t) * (size_t)P.kv_width;
   const int grid = ((P.n_units + 7) / 8) * 8;
   attend_kernel<D><<<grid, 128, smem, stream>>>(P);
   return hipGetLastError();
