@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--json-out", default=None)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="first run a plain 1 GiB device-to-device copy (known bytes) for counter scaling")
     return ap.parse_args()
 
 
@@ -81,6 +83,14 @@ def main():
         w = w.replace(q=a.q)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if a.calibrate_copy:
+        src = torch.empty(1 << 29, dtype=torch.int16, device=dev).fill_(1)   # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize(dev)
+        del src, dst
+        log("calibration copy: 2 x 1 GiB device-to-device")
     log(f"workload {w.name}: B={w.B} H={w.H}/{w.Hkv} d={w.d} N={w.N} k={w.k} q={w.q} backbone={w.backbone}")
     t0 = time.time()
     inp = synth.generate(w, threads=16)

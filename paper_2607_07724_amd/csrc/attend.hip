@@ -20,7 +20,8 @@
 //                 each lane ends up holding 16 keys of one query row.
 //   softmax       fp32 online softmax in base 2 (log2 e folded into the
 //                 scale); only the diagonal block t is masked (key > row);
-//                 the O rescale is skipped when no row max moved.
+//                 the reference max is raised only when a row max exceeds
+//                 it by more than 2^8, so O is rarely rescaled.
 //   O^T += V^T P^T  the lane's probabilities, packed to bf16, already are
 //                 the B operand; V^T comes straight from the natural-layout
 //                 LDS tile through the transposing read ds_read_b64_tr_b16
@@ -50,9 +51,12 @@ struct AttnParams {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// two fp32 -> packed bf16 pair (round to nearest even), one v_cvt_pk_bf16_f32
 __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-  const __bf16 x = (__bf16)a, y = (__bf16)b;
-  return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, bf16x2));
 }
 
 // s_waitcnt immediates (gfx9 encoding): vmcnt in bits 3:0 and 15:14,
@@ -84,35 +88,48 @@ struct Tile {
   __device__ static __forceinline__ int off(int r, int c) { return (r * CPR + (c ^ (r & (CPR - 1)))) * 8; }
 };
 
-// One direct-to-LDS 16-byte load per lane: M0 holds the wave-uniform LDS
-// destination, lane l's data lands at M0 + 16 l.  Issued from inline asm so
-// the compiler's wait-count insertion does not drain it before unrelated LDS
+// One direct-to-LDS 16-byte load per lane from base + voff (base is
+// wave-uniform, in SGPRs); M0 holds the wave-uniform LDS destination and
+// lane l's 16 bytes land at M0 + 16 l.  Issued from inline asm so the
+// compiler's wait-count insertion does not drain it before unrelated LDS
 // reads; the kernel waits on vmcnt explicitly (no other vector memory
 // operation is in flight while these are).
-__device__ __forceinline__ void dma16(const uint16_t* src, uint32_t lds_byte_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+__device__ __forceinline__ void dma16(const uint16_t* base, uint32_t voff, uint32_t lds_byte_addr) {
+  // M0 is written here and read by nothing else in these kernels (no
+  // indirect register moves, no GWS, no LDS parameter loads).
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
                :
-               : "v"(src), "s"(lds_byte_addr)
-               : "memory", "m0");
+               : "v"(voff), "s"(base), "s"(lds_byte_addr)
+               : "memory");
 }
 
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const LDS_AS void*)p;
 }
 
+// Byte offsets (within a block) of the chunks this lane moves: fixed for the
+// whole kernel, so they are computed once.
 template <int D>
-__device__ __forceinline__ void fetch_block(const uint16_t* src_blk, uint16_t* tile, int w, int lane) {
-  using L = Tile<D>;
-  const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr(tile));
+struct FetchPlan {
+  uint32_t voff[Tile<D>::kLoadsPerWave];
+  __device__ __forceinline__ void init(int w, int lane) {
+    using L = Tile<D>;
 #pragma unroll
-  for (int i = 0; i < L::kLoadsPerWave; ++i) {
-    const int inst = w * L::kLoadsPerWave + i;
-    const int p = inst * 64 + lane;                 // LDS chunk written by this lane
-    const int r = p / L::CPR;
-    const int c = (p % L::CPR) ^ (r & (L::CPR - 1));  // global chunk that belongs there
-    dma16(src_blk + r * D + c * 8, __builtin_amdgcn_readfirstlane(base + inst * 64 * 16));
+    for (int i = 0; i < L::kLoadsPerWave; ++i) {
+      const int inst = w * L::kLoadsPerWave + i;
+      const int p = inst * 64 + lane;                  // LDS chunk written by this lane
+      const int r = p / L::CPR;
+      const int c = (p % L::CPR) ^ (r & (L::CPR - 1));  // global chunk that belongs there
+      voff[i] = (uint32_t)((r * D + c * 8) * 2);
+    }
   }
-}
+  __device__ __forceinline__ void fetch(const uint16_t* src_blk, uint32_t tile_lds, int w) const {
+    using L = Tile<D>;
+#pragma unroll
+    for (int i = 0; i < L::kLoadsPerWave; ++i)
+      dma16(src_blk, voff[i], tile_lds + (uint32_t)((w * L::kLoadsPerWave + i) * 64 * 16));
+  }
+};
 
 template <int D>
 __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) attend_kernel(AttnParams P) {
@@ -126,7 +143,8 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
   __shared__ int s_n;
 
   const Shape& s = P.s;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform per wave
   const int g = lane >> 4, c16 = lane & 15;
   const int uid = xcd_remap(blockIdx.x, P.n_units);
   if (uid >= P.n_units) return;
@@ -171,9 +189,13 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
 
   const uint16_t* Kh = P.K + ((size_t)u.b * s.Hkv + kvh) * s.N * D;
   const uint16_t* Vh = P.V + ((size_t)u.b * s.Hkv + kvh) * s.N * D;
-  int blk = s_list[0];
-  fetch_block<D>(Kh + (size_t)blk * Tile<D>::kElems, s_k, w, lane);
-  fetch_block<D>(Vh + (size_t)blk * Tile<D>::kElems, s_v, w, lane);
+  FetchPlan<D> plan;
+  plan.init(w, lane);
+  const uint32_t k_lds = __builtin_amdgcn_readfirstlane(lds_addr(s_k));
+  const uint32_t v_lds = __builtin_amdgcn_readfirstlane(lds_addr(s_v));
+  int blk = __builtin_amdgcn_readfirstlane(s_list[0]);
+  plan.fetch(Kh + (size_t)blk * Tile<D>::kElems, k_lds, w);
+  plan.fetch(Vh + (size_t)blk * Tile<D>::kElems, v_lds, w);
 
   f32x4 acc_o[DT][2];
 #pragma unroll
@@ -185,7 +207,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
 
   for (int it = 0; it < n; ++it) {
     const bool has_next = it + 1 < n;
-    const int nblk = has_next ? s_list[it + 1] : 0;
+    const int nblk = has_next ? __builtin_amdgcn_readfirstlane(s_list[it + 1]) : 0;
 
     // K(it) landed (V(it) may still be in flight)
     wait_vmcnt<NW>();
@@ -210,29 +232,38 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
     wait_lgkm0();
     lds_barrier();                       // both waves are done reading s_k
-    if (has_next) fetch_block<D>(Kh + (size_t)nblk * Tile<D>::kElems, s_k, w, lane);
+    if (has_next) plan.fetch(Kh + (size_t)nblk * Tile<D>::kElems, k_lds, w);
 
-    // online softmax (base 2); lane holds row (32w + 16rt + c16), keys 16kt + 4g + i
-    const bool diag = (blk == u.t);
+    // online softmax (base 2); lane holds row (32w + 16rt + c16), keys 16kt + 4g + i.
+    // The reference max m_run only moves when a row max exceeds it by more
+    // than 2^8, so p <= 256 and O is rescaled rarely; O / l is unchanged.
+    if (blk == u.t) {                    // diagonal block: key > row is masked
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        const int r = 32 * w + 16 * rt + c16;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if ((16 * kt + 4 * g + i) > r) sc[kt][rt][i] = -__builtin_huge_valf();
+      }
+    }
     float alpha[2];
     uint32_t pb[2][2][4];
     bool moved = false;
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
-      const int r = 32 * w + 16 * rt + c16;
-      float mx = -__builtin_huge_valf();
+      float mx = fmaxf(fmaxf(sc[0][rt][0], sc[0][rt][1]), fmaxf(sc[0][rt][2], sc[0][rt][3]));
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (diag && (16 * kt + 4 * g + i) > r) sc[kt][rt][i] = -__builtin_huge_valf();
-          mx = fmaxf(mx, sc[kt][rt][i]);
-        }
+      for (int kt = 1; kt < 4; ++kt)
+        mx = fmaxf(mx, fmaxf(fmaxf(sc[kt][rt][0], sc[kt][rt][1]), fmaxf(sc[kt][rt][2], sc[kt][rt][3])));
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run[rt], mx * P.scale_log2);
-      moved |= m_new != m_run[rt];
-      alpha[rt] = __builtin_amdgcn_exp2f(m_run[rt] - m_new);
+      mx *= P.scale_log2;
+      const bool up = mx > m_run[rt] + 8.0f;
+      const float m_new = up ? mx : m_run[rt];
+      alpha[rt] = up ? __builtin_amdgcn_exp2f(m_run[rt] - m_new) : 1.0f;
+      moved |= up;
       m_run[rt] = m_new;
       float ls = 0.f;
       float p[4][4];
@@ -290,7 +321,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
     wait_lgkm0();
     lds_barrier();                       // both waves are done reading s_v
-    if (has_next) fetch_block<D>(Vh + (size_t)nblk * Tile<D>::kElems, s_v, w, lane);
+    if (has_next) plan.fetch(Vh + (size_t)nblk * Tile<D>::kElems, v_lds, w);
     blk = nblk;
   }
 
