@@ -1,0 +1,175 @@
+"""GPU parity at the full workload sizes (32K, 64K, 128K and layers of the
+28-layer stack), in the launch configuration the benchmark times.
+
+The whole problem runs on the GPU; the oracle recomputes sampled (batch,
+head, tile) units one by one from the same inputs:
+  - block metadata: every block, bit-exact;
+  - tile scores of sampled units: within the fp32 accumulation bound;
+  - selection of sampled rows given the oracle's scores: bit-exact;
+  - end-to-end sorted prefix of sampled rows: equal up to near-ties;
+  - route: properties that hold at any size (head mean in head order,
+    tau is the ceil(q n)-th smallest over the population, trigger set,
+    sentinel patch);
+  - attention on the oracle's kept list of sampled rows (both the top-k and
+    the expanded top-2k list): max-abs <= 2e-2, RMS <= 2e-3.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_07724_amd as ugbs
+from paper_2607_07724_amd import synth
+
+from gpu_helpers import attention_error, bf16_to_f64, dev, dev_bf16, host, host_bits, near_tie_ok
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+ATOL_MAX, ATOL_RMS = 2e-2, 2e-3
+BLK = 64
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need an MI355X; run them on the GPU box")
+    ugbs.lib()
+
+
+def sample_units(w, n, seed):
+    """Spread over tiles (early saturated tiles, the first population tile, the last tile) and heads."""
+    g = np.random.default_rng(seed)
+    ts = {0, 1, 2, w.k - 1, w.k, w.k + 1, w.T - 1, w.T // 2}
+    ts |= set(int(x) for x in g.integers(0, w.T, n))
+    units = [(int(g.integers(0, w.B)), int(g.integers(0, w.H)), t) for t in sorted(ts) if 0 <= t < w.T]
+    return np.array(units, np.int32)
+
+
+def run_full(w, layer=0, units_n=20):
+    torch = __import__("torch")
+    inp = synth.generate(w, layer=layer, threads=16)
+    p = ugbs.Problem.make(w.B, w.H, w.Hkv, w.N, w.d, w.k, w.q, w.backbone)
+    Q, K, V = dev_bf16(inp.Q), dev_bf16(inp.K), dev_bf16(inp.V)
+    bufs = ugbs.Buffers(p)
+    so = torch.empty((w.B, w.H, w.T, w.NB), dtype=torch.float32, device="cuda")
+    O = torch.empty_like(Q)
+    ugbs.prefill(p, Q, K, V, O, bufs, scores_out=so)
+    torch.cuda.synchronize()
+    units = sample_units(w, units_n, w.seed(layer))
+    return dict(w=w, inp=inp, p=p, Q=Q, K=K, V=V, bufs=bufs, so=so, units=units)
+
+
+def check_all(r):
+    torch = __import__("torch")
+    w, inp, p, bufs, units = r["w"], r["inp"], r["p"], r["bufs"], r["units"]
+    NB, k, T = w.NB, w.k, w.T
+    # ---- metadata: every block, bit-exact
+    meta = oracle.block_meta(w.backbone, inp.K, nthreads=16)
+    assert np.array_equal(host_bits(bufs.meta).reshape(meta.shape), meta)
+
+    # ---- tile scores of sampled units: fp32 accumulation bound
+    S = oracle.tile_scores(w.backbone, inp.Q, meta, w.Hkv, units=units, nthreads=16)
+    so = np.stack([host(r["so"][b, h, t]) for b, h, t in units])
+    fin = np.isfinite(S)
+    assert np.array_equal(fin, np.isfinite(so))
+    G = w.H // w.Hkv
+    KD = w.d * (2 if w.backbone == synth.QUEST else 1)
+    for i, (b, h, t) in enumerate(units):
+        if t < 2:
+            continue
+        q = np.abs(bf16_to_f64(inp.Q[b, h, t * BLK:(t + 1) * BLK]))
+        m = np.abs(bf16_to_f64(meta[b, h // G, 1:t]))
+        mm = np.maximum(m[:, 0], m[:, 1]) if m.shape[1] == 2 else m[:, 0]
+        bound = (q @ mm.T).max(axis=0) * KD * 2.0 ** -24 + 1e-30
+        err = np.abs(so[i, 1:t].astype(np.float64) - S[i, 1:t].astype(np.float64))
+        assert np.all(err <= bound), (b, h, t, float((err / bound).max()))
+
+    # ---- selection of sampled rows given the oracle's scores: bit-exact
+    ridx, rsig = oracle.select(S, k, t_of_row=units[:, 2])
+    sin = torch.zeros((w.B, w.H, T, NB), dtype=torch.float32, device="cuda")
+    for i, (b, h, t) in enumerate(units):
+        sin[b, h, t] = torch.from_numpy(S[i]).cuda()
+    idx2 = torch.empty_like(bufs.idx_sorted)
+    sig2 = torch.empty_like(bufs.sigma)
+    ugbs.ugbs_score_select(p, r["Q"], bufs.meta, idx2, sig2, scores_in=sin)
+    torch.cuda.synchronize()
+    for i, (b, h, t) in enumerate(units):
+        assert np.array_equal(host(idx2[b, h, t]), ridx[i]), (b, h, t)
+        assert host(sig2[b, h, t]).view(np.uint32) == rsig[i].view(np.uint32), (b, h, t)
+    del sin, idx2, sig2
+
+    # ---- end-to-end sorted prefix of sampled rows: equal up to near-ties
+    gidx = host(bufs.idx_sorted)
+    exempt = 0
+    for i, (b, h, t) in enumerate(units):
+        ok, nd = near_tie_ok(gidx[b, h, t], ridx[i], S[i], t, NB)
+        assert ok, (b, h, t, gidx[b, h, t], ridx[i])
+        exempt += nd > 0
+
+    # ---- route: properties at full size
+    sig = host(bufs.sigma)
+    sb = host(bufs.sigma_bar)
+    tau = host(bufs.tau)
+    trig = host(bufs.trigger).astype(bool)
+    kv = host(bufs.kv_idx)
+    P = oracle.population(T, k)
+    n = int(P.sum())
+    n_trig = math.ceil(w.q * n)
+    for b in range(w.B):
+        acc = np.zeros(T, np.float32)
+        for h in range(w.H):
+            acc = (acc + sig[b, h]).astype(np.float32)
+        mean = (acc / np.float32(w.H)).astype(np.float32)
+        assert np.array_equal(sb[b, P].view(np.uint32), mean[P].view(np.uint32))
+        assert np.all(sb[b, ~P] == -1) and np.all(sig[b][:, ~P] == -1)
+        assert np.all((sig[b][:, P] >= 0) & (sig[b][:, P] <= 1))
+        if n_trig:
+            vals = np.sort(sb[b, P])
+            assert tau[b] == vals[n_trig - 1]
+            assert np.array_equal(trig[b], P & (sb[b] <= tau[b]))
+            assert trig[b].sum() >= n_trig
+        else:
+            assert not trig[b].any()
+        exp_kv = gidx[b].copy()
+        exp_kv[:, ~trig[b], k:] = NB
+        assert np.array_equal(kv[b], exp_kv)
+    # sink and self always kept; sentinels trailing only
+    assert np.all(kv[..., 0] == 0)
+    assert np.all(kv[:, :, 1:, 1] == np.arange(1, T)[None, None, :])
+
+    # ---- attention on the oracle's kept lists of sampled rows
+    for width in (k, 2 * k):
+        rows = ridx.copy()
+        rows[:, width:] = NB
+        kvt = torch.full_like(bufs.kv_idx, NB)
+        for i, (b, h, t) in enumerate(units):
+            kvt[b, h, t] = torch.from_numpy(rows[i]).cuda()
+        O = torch.empty_like(r["Q"])
+        ugbs.ugbs_attend(p, r["Q"], r["K"], r["V"], kvt, O)
+        torch.cuda.synchronize()
+        ref = oracle.attend(inp.Q, inp.K, inp.V, kv_idx=rows, units=units, nthreads=16)
+        got = np.stack([host_bits(O[b, h, t * BLK:(t + 1) * BLK]) for b, h, t in units])
+        mx, rms = attention_error(got, ref)
+        assert mx <= ATOL_MAX and rms <= ATOL_RMS, (width, mx, rms)
+        del kvt, O
+    print(f"{w.name}: {len(units)} sampled units, near-tie exemptions {exempt}")
+
+
+@pytest.mark.parametrize("name", ["C2", "C3", "C4"])
+def test_full_size_workload(name):
+    r = run_full(synth.WORKLOADS[name])
+    check_all(r)
+
+
+@pytest.mark.parametrize("q", [0.05, 0.25])
+def test_full_size_128k_other_q(q):
+    r = run_full(synth.WORKLOADS["C4"].replace(q=q), units_n=12)
+    check_all(r)
+
+
+@pytest.mark.parametrize("layer,backbone", [(0, synth.KMEAN), (13, synth.QUEST), (27, synth.QUEST),
+                                            (27, synth.KMEAN)])
+def test_full_size_stack_layers(layer, backbone):
+    r = run_full(synth.WORKLOADS["C5"].replace(backbone=backbone), layer=layer, units_n=12)
+    check_all(r)
