@@ -1,7 +1,8 @@
 // Stages 2+3: tile scores, forcing, sorted top-2k and the cutoff margin
 // (A.2-A.6; Eqs. (tile-score), (sigma-def)).
 //
-// One wave per (batch, query head, Q-tile) unit.
+// One workgroup per (batch, kv head, Q-tile, group of up to 4 sibling query
+// heads); each wave owns one query head's unit (64 rows of tile t).
 //
 // Scoring is a dense contraction on bf16 MFMA (v_mfma_f32_16x16x32_bf16):
 //   S[64 rows x 16 blocks] = Qx[64 x KD] * Mx[KD x 16 blocks]
@@ -10,22 +11,31 @@
 //   max(q kmax, q kmin) = min(q,0) kmin + max(q,0) kmax,
 // so Qx = [q- | q+] and Mx = [kmin | kmax] (KD = 2d, the metadata row as
 // stored).  Every product is an exact bf16 x bf16 product; sums are fp32.
-// The 64-row Qx tile stays in registers as the A operand; metadata rows are
-// the B operand, loaded straight from global memory (they are shared by all
-// tiles of a kv head and stay L2-resident).  The max over the tile's rows
-// (A.3) is the max over a lane's 16 accumulators and then across the four
-// 16-lane groups.
+// The wave's 64-row Qx tile stays in registers as the A operand.  Metadata
+// rows (the B operand) come in chunks of 16 blocks that the workgroup's
+// waves fetch together with direct-to-LDS loads into a 4-slot ring (three
+// chunks in flight), so each chunk crosses L2 once per sibling group; in LDS
+// the 16-byte column c of row r sits at c ^ (r mod 16), which makes the
+// operand reads bank-conflict free.  The max over the tile's rows (A.3) is
+// the max over a lane's 16 accumulators and then across the four 16-lane
+// groups.
 //
-// Selection: tile scores become order-preserving 32-bit keys in LDS
-// (-0 folded into +0).  The R-th largest key (R = min(2k - |F|, |C|)) is found
-// by a most-significant-bit-first radix descent that counts with wave ballots,
-// the survivors are compacted (equal keys at the threshold by lower block
-// index), and a bitonic sort of (key, ~index) pairs orders them.  sigma uses
-// IEEE fp32 subtract and divide.
+// Selection (per wave, no workgroup barriers): tile scores become
+// order-preserving 32-bit keys (-0 folded into +0).  The R-th largest key
+// (R = min(2k - |F|, |C|)) is found by a most-significant-bit-first radix
+// descent that counts with wave ballots, the survivors are compacted (equal
+// keys at the threshold by lower block index), and a bitonic sort of
+// (key, ~index) pairs orders them.  sigma uses IEEE fp32 subtract and divide.
 #include "ugbs_internal.h"
 
 namespace ugbs {
 namespace {
+
+constexpr int kMaxGroup = 4;    // sibling query heads per workgroup
+constexpr int kRing = 4;        // metadata chunk slots (kRing - 1 in flight)
+constexpr int kChunk = 16;      // blocks per metadata chunk
+
+#define LDS_AS __attribute__((address_space(3)))
 
 struct SelParams {
   Shape s;
@@ -35,8 +45,12 @@ struct SelParams {
   float* scores_out;
   int32_t* idx_sorted;
   float* sigma;
-  int n_units;
-  int sel_cap;  // power of two >= max survivors
+  int GW;         // waves (query heads) per workgroup
+  int n_groups;   // head groups per kv head = ceil(G / GW)
+  int n_wg;       // workgroups
+  int sel_cap;    // power of two >= max survivors
+  int wave_lds;   // bytes of per-wave LDS (keys, then survivors)
+  int ring_lds;   // bytes of the metadata ring
 };
 
 __device__ __forceinline__ uint32_t order_key(float f) {
@@ -76,97 +90,186 @@ __device__ __forceinline__ float wave_max16(float v) {
   return v;
 }
 
-// Scores of candidate blocks 1..t-1 of one unit -> keys in s_key[blk - 1].
-template <int D, bool QUEST>
-__device__ __forceinline__ void score_unit(const SelParams& P, const Unit& u, int nc,
-                                           uint32_t* s_key) {
-  constexpr int KD = QUEST ? 2 * D : D;
-  constexpr int KS = KD / 32;
-  const Shape& s = P.s;
-  const int lane = threadIdx.x;
-  const int g = lane >> 4, c16 = lane & 15;
-  const int kvh = u.h / s.G;
+// LDS hand-off between lanes of one wave: LDS operations of a wave complete
+// in order, so waiting for this wave's outstanding ones is enough.
+__device__ __forceinline__ void wave_lds_sync() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_wave_barrier();
+}
 
-  // A operand: 4 row tiles x KS k-steps, 8 bf16 per lane each.
-  bf16x8 a[4][KS];
-  const uint16_t* qtile = P.Q + (((size_t)u.b * s.H + u.h) * s.N + (size_t)u.t * kBlock) * D;
-#pragma unroll
-  for (int rt = 0; rt < 4; ++rt) {
-    const uint16_t* qrow = qtile + (size_t)(16 * rt + c16) * D;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if constexpr (QUEST) {
-        const int kk = (ks % (D / 32)) * 32 + 8 * g;
-        const uint4 v = *reinterpret_cast<const uint4*>(qrow + kk);
-        a[rt][ks] = as_bf16x8(ks < D / 32 ? neg_part(v) : pos_part(v));
-      } else {
-        a[rt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g));
-      }
-    }
-  }
+// Workgroup barrier without a memory fence (the metadata ring's direct-to-LDS
+// fetches stay in flight); callers wait on vmcnt first.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
-  const uint16_t* mhead = P.meta + ((size_t)u.b * s.Hkv + kvh) * s.NB * KD;
-  const int nchunks = (nc + 15) / 16;
-  auto load_b = [&](int c, bf16x8* b) {
-    int blk = 1 + 16 * c + c16;
-    if (blk > nc) blk = 1;  // lanes past the last candidate read a valid row
-    const uint16_t* mrow = mhead + (size_t)blk * KD + 8 * g;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) b[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(mrow + 32 * ks));
-  };
-
-  bf16x8 bcur[KS], bnext[KS];
-  load_b(0, bcur);
-  for (int c = 0; c < nchunks; ++c) {
-    if (c + 1 < nchunks) load_b(c + 1, bnext);
-    f32x4 acc[4];
-#pragma unroll
-    for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt)
-        acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][ks], bcur[ks], acc[rt], 0, 0, 0);
-    float m = acc[0][0];
-#pragma unroll
-    for (int rt = 0; rt < 4; ++rt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) m = fmaxf(m, acc[rt][i]);
-    m = wave_max16(m);
-    const int pos = 16 * c + c16;
-    if (g == 0 && pos < nc) s_key[pos] = order_key(m);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) bcur[ks] = bnext[ks];
+// s_waitcnt vmcnt(n) for a wave-uniform runtime n (gfx9 encoding: vmcnt in
+// bits 3:0 and 15:14; expcnt and lgkmcnt left at "no wait").  n >= 32 (never
+// reached: at most 8 loads x 2 chunks) falls back to a full wait.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | 0x70 | 0xf00);
+}
+__device__ __forceinline__ void wait_vmcnt_dyn(int n) {
+  switch (n) {
+#define W_(N) case N: wait_vm<N>(); break;
+    W_(0) W_(1) W_(2) W_(3) W_(4) W_(5) W_(6) W_(7) W_(8) W_(9) W_(10) W_(11) W_(12) W_(13)
+    W_(14) W_(15) W_(16) W_(17) W_(18) W_(19) W_(20) W_(21) W_(22) W_(23) W_(24) W_(25)
+    W_(26) W_(27) W_(28) W_(29) W_(30) W_(31)
+#undef W_
+    default: wait_vm<0>(); break;
   }
 }
 
+// Direct-to-LDS 16-byte load per lane (see attend.hip): M0 = LDS
+// destination of lane 0, lane l lands at M0 + 16 l.  Hidden from the
+// compiler's wait-count insertion; waited on explicitly.
+__device__ __forceinline__ void dma16(const uint16_t* base, uint32_t voff, uint32_t lds_byte_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(base), "s"(lds_byte_addr)
+               : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const LDS_AS void*)p;
+}
+
 template <int D, bool QUEST>
-__global__ void __launch_bounds__(64) score_select_kernel(SelParams P) {
+struct MetaChunk {
+  static constexpr int KD = QUEST ? 2 * D : D;
+  static constexpr int CPR = KD / 8;                   // 16-byte columns per metadata row
+  static constexpr int SWZ = (CPR < 16 ? CPR : 16) - 1;
+  static constexpr int kBytes = kChunk * KD * 2;
+  static constexpr int kLoads = kBytes / 1024;         // 1 KiB direct loads per chunk
+  __device__ static __forceinline__ int off(int r, int c) { return (r * CPR + (c ^ (r & SWZ))) * 16; }
+};
+
+// Workgroup ordering: the id is XCD-remapped, then (b, kv head) outermost,
+// heaviest tile first, head groups innermost.
+struct Group {
+  int b, kvh, t, hg;
+};
+
+__device__ __forceinline__ Group group_of(int id, const SelParams& P) {
+  Group r;
+  r.hg = id % P.n_groups;
+  int rest = id / P.n_groups;
+  r.t = P.s.T - 1 - rest % P.s.T;
+  rest /= P.s.T;
+  r.kvh = rest % P.s.Hkv;
+  r.b = rest / P.s.Hkv;
+  return r;
+}
+
+template <int D, bool QUEST>
+__global__ void __launch_bounds__(64 * kMaxGroup) score_select_kernel(SelParams P) {
+  using MC = MetaChunk<D, QUEST>;
+  constexpr int KD = MC::KD;
+  constexpr int KS = KD / 32;
   extern __shared__ __align__(16) unsigned char smem[];
   const Shape& s = P.s;
-  uint32_t* s_key = reinterpret_cast<uint32_t*>(smem);                       // [NB]
-  uint64_t* s_sel = reinterpret_cast<uint64_t*>(smem + ((s.NB * 4 + 15) & ~15));  // [sel_cap]
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 4, c16 = lane & 15;
 
-  const int uid = xcd_remap(blockIdx.x, P.n_units);
-  if (uid >= P.n_units) return;
-  const Unit u = unit_of(uid, s);
-  const size_t row = ((size_t)u.b * s.H + u.h) * s.T + u.t;
-  const int nf = (u.t == 0) ? 1 : 2;
-  const int nc = (u.t >= 1) ? u.t - 1 : 0;
+  const int id = xcd_remap(blockIdx.x, P.n_wg);
+  if (id >= P.n_wg) return;
+  const Group gr = group_of(id, P);
+  const int hl = gr.hg * P.GW + w;                    // head within the kv head's group
+  const bool active = hl < s.G;
+  const int h = gr.kvh * s.G + (active ? hl : 0);
+  const int t = gr.t;
+  const size_t row = ((size_t)gr.b * s.H + h) * s.T + t;
+  const int nf = (t == 0) ? 1 : 2;
+  const int nc = (t >= 1) ? t - 1 : 0;
   const int m = s.k - nf;
   const int W = s.W;
   const int R = min(W - nf, nc);
 
-  if (nc > 0) {
-    if (P.scores_in) {
+  unsigned char* ring = smem;
+  uint32_t* s_key = reinterpret_cast<uint32_t*>(smem + P.ring_lds + w * P.wave_lds);  // [NB]
+  uint64_t* s_sel = reinterpret_cast<uint64_t*>(s_key);  // reused after the keys are in registers
+
+  if (nc > 0 && P.scores_in) {
+    if (active) {
       const float* src = P.scores_in + row * s.NB + 1;
       for (int p = lane; p < nc; p += 64) s_key[p] = order_key(src[p]);
-    } else {
-      score_unit<D, QUEST>(P, u, nc, s_key);
+    }
+  } else if (nc > 0) {
+    // ---- A operand: this wave's 64 query rows (Quest: [q- | q+]) ----------
+    bf16x8 a[4][KS];
+    const uint16_t* qtile = P.Q + (((size_t)gr.b * s.H + h) * s.N + (size_t)t * kBlock) * D;
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      const uint16_t* qrow = qtile + (size_t)(16 * rt + c16) * D;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if constexpr (QUEST) {
+          const int kk = (ks % (D / 32)) * 32 + 8 * g;
+          const uint4 v = *reinterpret_cast<const uint4*>(qrow + kk);
+          a[rt][ks] = as_bf16x8(ks < D / 32 ? neg_part(v) : pos_part(v));
+        } else {
+          a[rt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g));
+        }
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0x70 | 0xf00);  // vmcnt(0): Q is in registers
+
+    // ---- metadata ring: chunk c holds candidate blocks 1 + 16c .. 16c + 16
+    const uint16_t* mhead = P.meta + ((size_t)gr.b * s.Hkv + gr.kvh) * s.NB * KD;
+    const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(ring));
+    const int nchunks = (nc + kChunk - 1) / kChunk;
+    // this wave issues the chunk's 1 KiB loads i = w, w + GW, ...
+    const int n_mine = (MC::kLoads - w + P.GW - 1) / P.GW;
+    auto issue = [&](int c) {
+      const uint32_t slot = ring_lds + (uint32_t)((c % kRing) * MC::kBytes);
+      for (int i = w; i < MC::kLoads; i += P.GW) {
+        const int p = i * 64 + lane;                  // 16-byte LDS chunk of the slot
+        const int r = p / MC::CPR;                    // block row within the chunk
+        const int col = (p % MC::CPR) ^ (r & MC::SWZ);
+        // rows past the last candidate re-read the chunk's first row, which
+        // is a candidate (1 + 16c <= nc for every issued chunk)
+        const int rr = (1 + kChunk * c + r <= nc) ? r : 0;
+        const uint16_t* base = mhead + (size_t)__builtin_amdgcn_readfirstlane(1 + kChunk * c) * KD;
+        dma16(base, (uint32_t)((rr * KD + col * 8) * 2), __builtin_amdgcn_readfirstlane(slot + i * 1024));
+      }
+    };
+    for (int c = 0; c < kRing - 1 && c < nchunks; ++c) issue(c);
+
+    for (int c = 0; c < nchunks; ++c) {
+      const int after = min(kRing - 2, nchunks - 1 - c);  // chunks issued after c
+      wait_vmcnt_dyn(n_mine * after);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of chunk c-1 are done
+      lds_barrier();                                    // chunk c landed; chunk c-1 is free
+      if (c + kRing - 1 < nchunks) issue(c + kRing - 1);
+      if (active) {
+        const unsigned char* slot = ring + (c % kRing) * MC::kBytes;
+        f32x4 acc[4];
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8 b = as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(c16, 4 * ks + g)));
+#pragma unroll
+          for (int rt = 0; rt < 4; ++rt)
+            acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][ks], b, acc[rt], 0, 0, 0);
+        }
+        float mx = acc[0][0];
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, acc[rt][i]);
+        mx = wave_max16(mx);
+        const int pos = kChunk * c + c16;
+        if (g == 0 && pos < nc) s_key[pos] = order_key(mx);
+      }
     }
   }
-  __syncthreads();
+  if (!active) return;
+  wave_lds_sync();
 
   if (P.scores_out) {
     float* dst = P.scores_out + row * s.NB;
@@ -176,7 +279,7 @@ __global__ void __launch_bounds__(64) score_select_kernel(SelParams P) {
 
   int32_t* out = P.idx_sorted + row * W;
   if (nc == 0) {
-    for (int p = lane; p < W; p += 64) out[p] = (p < nf) ? (p == 0 ? 0 : u.t) : s.NB;
+    for (int p = lane; p < W; p += 64) out[p] = (p < nf) ? (p == 0 ? 0 : t) : s.NB;
     if (lane == 0) P.sigma[row] = -1.0f;
     return;
   }
@@ -190,6 +293,7 @@ __global__ void __launch_bounds__(64) score_select_kernel(SelParams P) {
     const int p = 64 * sl + lane;
     keys[sl] = (sl < nslots && p < nc) ? s_key[p] : 0u;  // valid keys are >= 0x007fffff
   }
+  wave_lds_sync();                                       // s_key is reused for survivors below
   uint32_t thr = 0;
   bool exact = false;
   for (int bit = 31; bit >= 0; --bit) {
@@ -243,7 +347,7 @@ __global__ void __launch_bounds__(64) score_select_kernel(SelParams P) {
   int n2 = 2;
   while (n2 < R) n2 <<= 1;
   for (int p = R + lane; p < n2; p += 64) s_sel[p] = 0ull;
-  __syncthreads();
+  wave_lds_sync();
 
   // ---- bitonic sort, descending -------------------------------------------
   for (int size = 2; size <= n2; size <<= 1) {
@@ -258,7 +362,7 @@ __global__ void __launch_bounds__(64) score_select_kernel(SelParams P) {
           s_sel[hi] = x;
         }
       }
-      __syncthreads();
+      wave_lds_sync();
     }
   }
 
@@ -266,7 +370,7 @@ __global__ void __launch_bounds__(64) score_select_kernel(SelParams P) {
   for (int p = lane; p < W; p += 64) {
     int v;
     if (p < nf)
-      v = (p == 0) ? 0 : u.t;
+      v = (p == 0) ? 0 : t;
     else if (p - nf < R)
       v = 1 + (int)(0xffffffffu - (uint32_t)(s_sel[p - nf] & 0xffffffffu));
     else
@@ -289,10 +393,17 @@ __global__ void __launch_bounds__(64) score_select_kernel(SelParams P) {
 }
 
 template <int D, bool QUEST>
-hipError_t launch_t(const SelParams& P, hipStream_t stream) {
-  const size_t smem = ((P.s.NB * 4 + 15) & ~15) + sizeof(uint64_t) * (size_t)P.sel_cap;
-  const int grid = ((P.n_units + 7) / 8) * 8;
-  score_select_kernel<D, QUEST><<<grid, 64, smem, stream>>>(P);
+hipError_t launch_t(SelParams P, hipStream_t stream) {
+  using MC = MetaChunk<D, QUEST>;
+  P.ring_lds = kRing * MC::kBytes;
+  const size_t smem = (size_t)P.ring_lds + (size_t)P.GW * P.wave_lds;
+  if (smem > 65536) {  // large budgets (k near N_B): raise the dynamic-LDS limit
+    const hipError_t e = hipFuncSetAttribute((const void*)score_select_kernel<D, QUEST>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+  }
+  const int grid = ((P.n_wg + 7) / 8) * 8;
+  score_select_kernel<D, QUEST><<<grid, 64 * P.GW, smem, stream>>>(P);
   return hipGetLastError();
 }
 
@@ -309,11 +420,17 @@ hipError_t launch_score_select(const Shape& s, const uint16_t* Q, const uint16_t
   P.scores_out = scores_out;
   P.idx_sorted = idx_sorted;
   P.sigma = sigma;
-  P.n_units = s.B * s.H * s.T;
+  P.GW = s.G < kMaxGroup ? s.G : kMaxGroup;
+  P.n_groups = (s.G + P.GW - 1) / P.GW;
+  P.n_wg = s.B * s.Hkv * s.T * P.n_groups;
   int cap = 2;
   const int rmax = s.W < s.NB ? s.W : s.NB;
   while (cap < rmax) cap <<= 1;
   P.sel_cap = cap;
+  const int key_bytes = ((s.NB * 4 + 15) & ~15);
+  const int sel_bytes = 8 * cap;
+  P.wave_lds = key_bytes > sel_bytes ? key_bytes : sel_bytes;
+  P.ring_lds = 0;
   if (s.d == 128)
     return s.backbone == UGBS_QUEST ? launch_t<128, true>(P, stream) : launch_t<128, false>(P, stream);
   return s.backbone == UGBS_QUEST ? launch_t<64, true>(P, stream) : launch_t<64, false>(P, stream);
