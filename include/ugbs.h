@@ -159,9 +159,9 @@ UGBS_API int ugbs_route(const ugbs_problem* p, const float* sigma, const int32_t
  *   J_i = { j <= i : block(j) is listed in kv_idx[b, h, t, :] } and
  *   O_i = sum_{j in J_i} softmax_j(scale * q_i . k_j) v_j, computed with bf16
  *   products, fp32 accumulation and an fp32 online softmax.  Entries outside
- *   [0, N_B) (the sentinel N_B included) and blocks after t are skipped.
- *   Entries of a row must be distinct (a repeated block is undefined, but
- *   is never read out of bounds).  A row with no attended key gives O = 0.
+ *   [0, N_B) (the sentinel N_B included) and blocks after t are skipped, and
+ *   a block listed twice counts once (the row is a set, as in J_i).  A row
+ *   with no attended key gives O = 0.
  *   kv_idx with every block 0..t listed (kv_width = N_B) is dense causal
  *   attention.
  *   Q, K, V : as in the conventions above, 16-byte aligned.

@@ -2,8 +2,8 @@
 //
 // One workgroup of two waves per (batch, query head, Q-tile) unit; wave w
 // owns query rows 32w..32w+31 of the tile.  The tile's kv_idx row is first
-// compacted into LDS (entries outside 0..t are dropped, order kept), then
-// the listed key blocks are visited one by one.
+// turned into an ascending list of distinct blocks in 0..t (so the diagonal
+// block comes last), then the listed key blocks are visited one by one.
 //
 // Staging.  K and V blocks (64 keys x d, bf16) go global -> LDS with
 // direct-to-LDS loads (global_load_lds_dwordx4: no registers, no VALU).
@@ -17,7 +17,9 @@
 // Compute, per block and wave (v_mfma_f32_16x16x32_bf16):
 //   S^T = K Q^T   K rows from LDS (ds_read_b128) are the A operand; the
 //                 wave's 32 query rows stay in registers as the B operand;
-//                 each lane ends up holding 16 keys of one query row.
+//                 each lane ends up holding 16 keys of one query row.  S of
+//                 the next block is issued together with the softmax of the
+//                 current one, so the matrix cores and the VALU overlap.
 //   softmax       fp32 online softmax in base 2 (log2 e folded into the
 //                 scale); only the diagonal block t is masked (key > row);
 //                 the reference max is raised only when a row max exceeds
@@ -28,6 +30,8 @@
 //                 (16 lanes fetch a 4-key x 16-channel patch and each lane
 //                 receives the 4 keys of one channel).
 // Per listed block and unit: 4*64*64*d FLOP on 2*64*d*2 bytes of K/V.
+#include <type_traits>
+
 #include "ugbs_internal.h"
 
 namespace ugbs {
@@ -74,8 +78,20 @@ __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xc07f
 // operations across it.
 __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
   __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
   asm volatile("" ::: "memory");
+}
+
+// max over the four 16-lane rows holding one query row (lanes l, l^16,
+// l^32, l^48) with the gfx950 row-swap permutes (VALU, no LDS round trip):
+// permlane32_swap pairs row r with row r^2, permlane16_swap row r with r^1.
+__device__ __forceinline__ float rows_max(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
 template <int D>
@@ -139,7 +155,8 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
   constexpr int NW = L::kLoadsPerWave;
   __shared__ __align__(16) uint16_t s_k[L::kElems];
   __shared__ __align__(16) uint16_t s_v[L::kElems];
-  extern __shared__ int32_t s_list[];
+  extern __shared__ int32_t s_list[];          // [kv_width]: at most kv_width distinct blocks
+  __shared__ uint32_t s_bits[UGBS_MAX_BLOCKS / 32];
   __shared__ int s_n;
 
   const Shape& s = P.s;
@@ -152,17 +169,31 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int kvh = u.h / s.G;
   const size_t rowid = ((size_t)u.b * s.H + u.h) * s.T + u.t;
 
-  // ---- compact the kv_idx row (wave 0), preserving slot order -------------
+  // ---- the tile's kept blocks, ascending (wave 0): kv_idx entries outside
+  // 0..t are dropped and repeated entries count once (set semantics, as in
+  // Eq. (Attn)); ascending order puts the diagonal block t last (the only one
+  // needing the causal mask) and lets units that run side by side on an XCD
+  // sweep the key range together, so blocks they share are L2 hits.
   if (w == 0) {
     const int32_t* kr = P.kv_idx + rowid * P.kv_width;
-    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    int n = 0;
+    const int nwords = (u.t >> 5) + 1;                 // bitmap words covering blocks 0..t
+    for (int i = lane; i < nwords; i += 64) s_bits[i] = 0u;
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
     for (int base = 0; base < P.kv_width; base += 64) {
       const int sl = base + lane;
       const int blk = (sl < P.kv_width) ? kr[sl] : -1;
-      const bool ok = blk >= 0 && blk <= u.t;
-      const uint64_t m = __ballot(ok);
-      if (ok) s_list[n + __popcll(m & lt)] = blk;
+      if (blk >= 0 && blk <= u.t) atomicOr(&s_bits[blk >> 5], 1u << (blk & 31));
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    int n = 0;
+    for (int base = 0; base <= u.t; base += 64) {
+      const int blk = base + lane;
+      const bool on = blk <= u.t && ((s_bits[blk >> 5] >> (blk & 31)) & 1u);
+      const uint64_t m = __ballot(on);
+      if (on) s_list[n + __popcll(m & lt)] = blk;
       n += __popcll(m);
     }
     if (lane == 0) s_n = n;
@@ -193,9 +224,6 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
   plan.init(w, lane);
   const uint32_t k_lds = __builtin_amdgcn_readfirstlane(lds_addr(s_k));
   const uint32_t v_lds = __builtin_amdgcn_readfirstlane(lds_addr(s_v));
-  int blk = __builtin_amdgcn_readfirstlane(s_list[0]);
-  plan.fetch(Kh + (size_t)blk * Tile<D>::kElems, k_lds, w);
-  plan.fetch(Vh + (size_t)blk * Tile<D>::kElems, v_lds, w);
 
   f32x4 acc_o[DT][2];
 #pragma unroll
@@ -205,16 +233,8 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
   float m_run[2] = {-__builtin_huge_valf(), -__builtin_huge_valf()};
   float l_run[2] = {0.f, 0.f};
 
-  for (int it = 0; it < n; ++it) {
-    const bool has_next = it + 1 < n;
-    const int nblk = has_next ? __builtin_amdgcn_readfirstlane(s_list[it + 1]) : 0;
-
-    // K(it) landed (V(it) may still be in flight)
-    wait_vmcnt<NW>();
-    lds_barrier();
-
-    // S^T = K Q^T : [64 keys x 32 rows] per wave
-    f32x4 sc[4][2];
+  // S^T = K Q^T : [64 keys x 32 rows] per wave, K from LDS
+  auto compute_s = [&](f32x4 (&sc)[4][2]) {
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
@@ -230,14 +250,43 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
           sc[kt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, bq[rt][ks], sc[kt][rt], 0, 0, 0);
       }
     }
-    wait_lgkm0();
-    lds_barrier();                       // both waves are done reading s_k
-    if (has_next) plan.fetch(Kh + (size_t)nblk * Tile<D>::kElems, k_lds, w);
+  };
 
-    // online softmax (base 2); lane holds row (32w + 16rt + c16), keys 16kt + 4g + i.
-    // The reference max m_run only moves when a row max exceeds it by more
-    // than 2^8, so p <= 256 and O is rescaled rarely; O / l is unchanged.
-    if (blk == u.t) {                    // diagonal block: key > row is masked
+  // Pipeline per listed block i (K and V have one LDS buffer each):
+  //   S(i+1) on the matrix cores overlaps the softmax of S(i) on the VALU,
+  //   then O += P(i) V(i).  K(i+2) is fetched once S(i+1) is done, V(i+1)
+  //   once PV(i) is done.  Fetch order per wave: K0 V0 K1 | K2 V1 | K3 V2 ...
+  int blk = __builtin_amdgcn_readfirstlane(s_list[0]);
+  plan.fetch(Kh + (size_t)blk * Tile<D>::kElems, k_lds, w);
+  plan.fetch(Vh + (size_t)blk * Tile<D>::kElems, v_lds, w);
+  f32x4 sc[4][2];
+  wait_vmcnt<NW>();                      // K0 landed
+  lds_barrier();
+  compute_s(sc);
+  wait_lgkm0();
+  lds_barrier();                         // both waves are done reading s_k
+  if (n > 1) plan.fetch(Kh + (size_t)__builtin_amdgcn_readfirstlane(s_list[1]) * Tile<D>::kElems, k_lds, w);
+
+  // One pipeline step for listed block `it`; MASK: it is the diagonal block
+  // (always the last one), whose keys after the query row are masked.
+  auto step = [&](int it, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    const bool has_next = it + 1 < n;
+    const bool has_next2 = it + 2 < n;
+    const int nblk = has_next ? __builtin_amdgcn_readfirstlane(s_list[it + 1]) : 0;
+
+    if (has_next) {                      // K(it+1) landed (V(it) may be in flight)
+      if (it == 0) wait_vmcnt<0>(); else wait_vmcnt<NW>();
+      lds_barrier();
+    }
+    // S(it+1): on the last block this re-reads s_k (no fetch is pending) and is discarded
+    f32x4 sn[4][2];
+    compute_s(sn);
+
+    // online softmax of S(it) (base 2); lane holds row (32w + 16rt + c16),
+    // keys 16kt + 4g + i.  The reference max m_run only moves when a row max
+    // exceeds it by more than 2^8, so p <= 256 and O is rescaled rarely.
+    if constexpr (MASK) {
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt) {
         const int r = 32 * w + 16 * rt + c16;
@@ -257,9 +306,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
       for (int kt = 1; kt < 4; ++kt)
         mx = fmaxf(mx, fmaxf(fmaxf(sc[kt][rt][0], sc[kt][rt][1]), fmaxf(sc[kt][rt][2], sc[kt][rt][3])));
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      mx *= P.scale_log2;
+      mx = rows_max(mx) * P.scale_log2;
       const bool up = mx > m_run[rt] + 8.0f;
       const float m_new = up ? mx : m_run[rt];
       alpha[rt] = up ? __builtin_amdgcn_exp2f(m_run[rt] - m_new) : 1.0f;
@@ -283,6 +330,29 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
         pb[rt][j][3] = pack_bf16(p[2 * j + 1][2], p[2 * j + 1][3]);
       }
     }
+    // interleave, in two halves: 8 K-operand reads, then one MFMA of
+    // S(it+1) per five softmax VALU instructions
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+      }
+    }
+
+    if (has_next) {
+      wait_lgkm0();
+      lds_barrier();                     // both waves are done reading s_k
+      if (has_next2)
+        plan.fetch(Kh + (size_t)__builtin_amdgcn_readfirstlane(s_list[it + 2]) * Tile<D>::kElems, k_lds, w);
+    }
+
+    // V(it) landed (K(it+2) may still be in flight)
+    if (has_next2) wait_vmcnt<NW>(); else wait_vmcnt<0>();
+    lds_barrier();
+
     if (__ballot(moved)) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
@@ -291,10 +361,6 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
           for (int i = 0; i < 4; ++i) acc_o[dt][rt][i] *= alpha[rt];
     }
-
-    // V(it) landed (K(it+1) may still be in flight)
-    if (has_next) wait_vmcnt<NW>(); else wait_vmcnt<0>();
-    lds_barrier();
 
     // O^T += V^T P^T ; lane (channel 16dt + c16, group g) takes keys
     // 32j + 4g + 0..3 and 32j + 16 + 4g + 0..3 through two transposing reads
@@ -322,8 +388,16 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
     wait_lgkm0();
     lds_barrier();                       // both waves are done reading s_v
     if (has_next) plan.fetch(Vh + (size_t)nblk * Tile<D>::kElems, v_lds, w);
-    blk = nblk;
-  }
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) sc[kt][rt] = sn[kt][rt];
+  };
+
+  const bool diag_last = s_list[n - 1] == u.t;
+  for (int it = 0; it + 1 < n; ++it) step(it, std::false_type{});
+  if (diag_last) step(n - 1, std::true_type{});
+  else step(n - 1, std::false_type{});
 
   // ---- normalise and store: lane holds O^T[16dt + 4g + i][row] ------------
 #pragma unroll

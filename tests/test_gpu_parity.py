@@ -240,6 +240,18 @@ def test_attention_random_rows_with_junk_entries_and_custom_scale(name):
         assert mx <= ATOL_MAX and rms <= ATOL_RMS, (W, mx, rms)
 
 
+def test_attention_repeated_blocks_count_once():
+    c = case("kmean_d128_gqa4")
+    w, inp = c["w"], c["inp"]
+    kv = synth.random_kv_idx(77, w.B, w.H, w.T, 5, shuffle=True)
+    dup = np.concatenate([kv, kv[..., ::-1]], axis=-1)   # every entry listed twice
+    assert (dup[..., :5] == dup[..., 5:][..., ::-1]).all()
+    O = _attend_gpu(w, inp, dup)
+    ref = oracle.attend(inp.Q, inp.K, inp.V, kv_idx=dup)  # the oracle's rows are sets
+    mx, rms = attention_error(O, ref)
+    assert mx <= ATOL_MAX and rms <= ATOL_RMS, (mx, rms)
+
+
 def test_attention_empty_rows_give_zero():
     c = case("C1")
     w, inp = c["w"], c["inp"]
