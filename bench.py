@@ -41,7 +41,7 @@ def parse():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--json-out", default=None)
     ap.add_argument("--calibrate-copy", action="store_true",
-                    help="first run a plain 1 GiB device-to-device copy (known bytes) for counter scaling")
+                    help="first run a plain streaming kernel (1 GiB in, 1 GiB out) to scale HBM counters")
     return ap.parse_args()
 
 
@@ -84,13 +84,14 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     if a.calibrate_copy:
-        src = torch.empty(1 << 29, dtype=torch.int16, device=dev).fill_(1)   # 1 GiB
+        # a plain streaming kernel of known size: reads 1 GiB, writes 1 GiB
+        src = torch.empty(1 << 29, dtype=torch.int16, device=dev).fill_(1)
         dst = torch.empty_like(src)
         for _ in range(2):
-            dst.copy_(src)
+            torch.add(src, 1, out=dst)
         torch.cuda.synchronize(dev)
         del src, dst
-        log("calibration copy: 2 x 1 GiB device-to-device")
+        log("calibration: 2 x elementwise add, 1 GiB read + 1 GiB written each")
     log(f"workload {w.name}: B={w.B} H={w.H}/{w.Hkv} d={w.d} N={w.N} k={w.k} q={w.q} backbone={w.backbone}")
     t0 = time.time()
     inp = synth.generate(w, threads=16)

@@ -21,11 +21,15 @@
 // groups.
 //
 // Selection (per wave, no workgroup barriers): tile scores become
-// order-preserving 32-bit keys (-0 folded into +0).  The R-th largest key
-// (R = min(2k - |F|, |C|)) is found by a most-significant-bit-first radix
-// descent that counts with wave ballots, the survivors are compacted (equal
-// keys at the threshold by lower block index), and a bitonic sort of
-// (key, ~index) pairs orders them.  sigma uses IEEE fp32 subtract and divide.
+// order-preserving 32-bit keys (-0 folded into +0).  A per-lane top-2
+// pre-filter bounds the R-th largest key from below (R = min(2k - |F|, |C|)),
+// the R-th largest key is found among the survivors by a
+// most-significant-bit-first radix descent that counts with wave ballots,
+// the top R are compacted (equal keys at the threshold by lower block
+// index) and ordered by (key, ~index): for R <= 128 each survivor's rank is
+// counted in registers from readlane broadcasts and it is scattered into
+// place, otherwise a bitonic sort in LDS.  sigma uses IEEE fp32 subtract and
+// divide.
 #include "ugbs_internal.h"
 
 namespace ugbs {
@@ -84,10 +88,75 @@ __device__ __forceinline__ uint4 pos_part(uint4 v) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-__device__ __forceinline__ float wave_max16(float v) {
-  v = fmaxf(v, __shfl_xor(v, 16));
-  v = fmaxf(v, __shfl_xor(v, 32));
-  return v;
+// max over the four 16-lane rows (lanes l, l^16, l^32, l^48) with the gfx950
+// row-swap permutes: permlane32_swap pairs row r with r^2, permlane16_swap
+// row r with r^1 (VALU only, no LDS round trip).
+__device__ __forceinline__ float wave_max16(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+constexpr int kSurvivors = 256;   // pre-filter survivors handled in registers
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = min(x, (uint32_t)__shfl_xor((int)x, o));
+  return x;
+}
+
+// R largest of the keys held in key[0..nslots) (0 = empty; entries in
+// position order slot by slot, lane by lane), written to s_sel[0..R) as
+// (key << 32) | ~position, unsorted: a most-significant-bit-first radix
+// descent finds the R-th largest key thr by counting with wave ballots,
+// then keys above thr and the lowest-position keys equal to thr are
+// compacted.
+template <int S>
+__device__ __forceinline__ void select_top(const uint32_t (&key)[S], const uint32_t (&pos)[S],
+                                           int nslots, int R, uint64_t* s_sel, int lane) {
+  uint32_t thr = 0;
+  bool exact = false;
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t cand = thr | (1u << bit);
+    int cnt = 0;
+#pragma unroll
+    for (int sl = 0; sl < S; ++sl)
+      if (sl < nslots) cnt += __popcll(__ballot(key[sl] >= cand));
+    if (cnt >= R) {
+      thr = cand;
+      if (cnt == R) {
+        exact = true;
+        break;
+      }
+    }
+  }
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  int base = 0;
+#pragma unroll
+  for (int sl = 0; sl < S; ++sl) {
+    if (sl < nslots) {
+      const bool take = exact ? (key[sl] >= thr) : (key[sl] > thr);
+      const uint64_t mk = __ballot(take);
+      if (take) s_sel[base + __popcll(mk & lt_mask)] = ((uint64_t)key[sl] << 32) | (0xffffffffu - pos[sl]);
+      base += __popcll(mk);
+    }
+  }
+  if (!exact) {
+    int need = R - base;
+#pragma unroll
+    for (int sl = 0; sl < S; ++sl) {
+      if (sl < nslots && need > 0) {
+        const bool eq = key[sl] == thr;
+        const uint64_t mk = __ballot(eq);
+        const int r = __popcll(mk & lt_mask);
+        if (eq && r < need) s_sel[base + r] = ((uint64_t)thr << 32) | (0xffffffffu - pos[sl]);
+        const int took = min(__popcll(mk), need);
+        base += took;
+        need -= took;
+      }
+    }
+  }
 }
 
 // LDS hand-off between lanes of one wave: LDS operations of a wave complete
@@ -224,17 +293,33 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_select_kernel(SelParams 
     const int nchunks = (nc + kChunk - 1) / kChunk;
     // this wave issues the chunk's 1 KiB loads i = w, w + GW, ...
     const int n_mine = (MC::kLoads - w + P.GW - 1) / P.GW;
+    // this wave's share of a chunk: loads i = w, w + GW, ... (at most 8);
+    // lane offsets within the chunk are fixed, only the base moves
+    constexpr int kMaxMine = MC::kLoads;
+    uint32_t voff[kMaxMine], vrow[kMaxMine];
+#pragma unroll
+    for (int j = 0; j < kMaxMine; ++j) {
+      const int i = w + j * P.GW;
+      const int p = i * 64 + lane;                    // 16-byte LDS chunk of the slot
+      const int r = p / MC::CPR;                      // block row within the chunk
+      const int col = (p % MC::CPR) ^ (r & MC::SWZ);
+      vrow[j] = (uint32_t)r;
+      voff[j] = (uint32_t)((r * KD + col * 8) * 2);
+    }
     auto issue = [&](int c) {
       const uint32_t slot = ring_lds + (uint32_t)((c % kRing) * MC::kBytes);
-      for (int i = w; i < MC::kLoads; i += P.GW) {
-        const int p = i * 64 + lane;                  // 16-byte LDS chunk of the slot
-        const int r = p / MC::CPR;                    // block row within the chunk
-        const int col = (p % MC::CPR) ^ (r & MC::SWZ);
-        // rows past the last candidate re-read the chunk's first row, which
-        // is a candidate (1 + 16c <= nc for every issued chunk)
-        const int rr = (1 + kChunk * c + r <= nc) ? r : 0;
-        const uint16_t* base = mhead + (size_t)__builtin_amdgcn_readfirstlane(1 + kChunk * c) * KD;
-        dma16(base, (uint32_t)((rr * KD + col * 8) * 2), __builtin_amdgcn_readfirstlane(slot + i * 1024));
+      const uint16_t* base = mhead + (size_t)__builtin_amdgcn_readfirstlane(1 + kChunk * c) * KD;
+      const bool last = kChunk * (c + 1) >= nc;       // wave-uniform
+#pragma unroll
+      for (int j = 0; j < kMaxMine; ++j) {
+        const int i = w + j * P.GW;
+        if (i < MC::kLoads) {
+          // rows past the last candidate re-read the chunk's first row, which
+          // is a candidate (1 + 16c <= nc for every issued chunk)
+          uint32_t off = voff[j];
+          if (last && 1 + kChunk * c + (int)vrow[j] > nc) off -= vrow[j] * (uint32_t)(KD * 2);
+          dma16(base, off, __builtin_amdgcn_readfirstlane(slot + i * 1024));
+        }
       }
     };
     for (int c = 0; c < kRing - 1 && c < nchunks; ++c) issue(c);
@@ -284,7 +369,12 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_select_kernel(SelParams 
     return;
   }
 
-  // ---- R-th largest key by radix descent over the 32 key bits -------------
+  // ---- the R largest keys, compacted into s_sel as (key, ~position) -------
+  // Pre-filter: with P = ceil(R / 64) <= 2, the smallest over lanes of each
+  // lane's P-th largest key, T0, has at least 64 P >= R keys at or above it,
+  // so the R largest are among {key >= T0} (typically a few hundred of up to
+  // 2046).  Those survivors, in position order, go through the exact
+  // selection; otherwise every candidate does.
   constexpr int kMaxSlots = UGBS_MAX_BLOCKS / 64;
   const int nslots = (nc + 63) / 64;
   uint32_t keys[kMaxSlots];
@@ -294,75 +384,95 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_select_kernel(SelParams 
     keys[sl] = (sl < nslots && p < nc) ? s_key[p] : 0u;  // valid keys are >= 0x007fffff
   }
   wave_lds_sync();                                       // s_key is reused for survivors below
-  uint32_t thr = 0;
-  bool exact = false;
-  for (int bit = 31; bit >= 0; --bit) {
-    const uint32_t cand = thr | (1u << bit);
-    int cnt = 0;
-#pragma unroll
-    for (int sl = 0; sl < kMaxSlots; ++sl)
-      if (sl < nslots) cnt += __popcll(__ballot(keys[sl] >= cand));
-    if (cnt >= R) {
-      thr = cand;
-      if (cnt == R) {
-        exact = true;
-        break;
-      }
-    }
-  }
-
-  // ---- compact the survivors as (key, ~position) pairs --------------------
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  int base = 0;
-#pragma unroll
-  for (int sl = 0; sl < kMaxSlots; ++sl) {
-    if (sl < nslots) {
-      const bool take = exact ? (keys[sl] >= thr) : (keys[sl] > thr);
-      const uint64_t mk = __ballot(take);
-      if (take) {
-        const uint32_t pos = 64 * sl + lane;
-        s_sel[base + __popcll(mk & lt_mask)] = ((uint64_t)keys[sl] << 32) | (0xffffffffu - pos);
-      }
-      base += __popcll(mk);
-    }
-  }
-  if (!exact) {
-    int need = R - base;
+  bool filtered = false;
+  if (R <= 128 && nc > R) {
+    uint32_t m1 = 0, m2 = 0;
 #pragma unroll
     for (int sl = 0; sl < kMaxSlots; ++sl) {
-      if (sl < nslots && need > 0) {
-        const bool eq = keys[sl] == thr;
-        const uint64_t mk = __ballot(eq);
-        const int r = __popcll(mk & lt_mask);
-        if (eq && r < need) {
-          const uint32_t pos = 64 * sl + lane;
-          s_sel[base + r] = ((uint64_t)thr << 32) | (0xffffffffu - pos);
+      if (sl < nslots) {
+        const uint32_t x = keys[sl];
+        const uint32_t lo = min(m1, x);
+        m1 = max(m1, x);
+        m2 = max(m2, lo);
+      }
+    }
+    uint32_t t0 = (R <= 64) ? m1 : m2;
+    t0 = wave_min_u32(t0);
+    if (t0 > 0u) {
+      int ns = 0;
+#pragma unroll
+      for (int sl = 0; sl < kMaxSlots; ++sl) {
+        if (sl < nslots) {
+          const bool take = keys[sl] >= t0;
+          const uint64_t mk = __ballot(take);
+          const int at = ns + __popcll(mk & lt_mask);
+          if (take && at < kSurvivors)
+            s_sel[at] = ((uint64_t)keys[sl] << 32) | (uint32_t)(64 * sl + lane);
+          ns += __popcll(mk);
         }
-        const int took = min(__popcll(mk), need);
-        base += took;
-        need -= took;
+      }
+      if (ns <= kSurvivors) {
+        wave_lds_sync();
+        uint32_t k2[kSurvivors / 64], p2[kSurvivors / 64];
+#pragma unroll
+        for (int sl = 0; sl < kSurvivors / 64; ++sl) {
+          const int i = 64 * sl + lane;
+          const uint64_t v = (i < ns) ? s_sel[i] : 0ull;
+          k2[sl] = (uint32_t)(v >> 32);
+          p2[sl] = (uint32_t)v;
+        }
+        wave_lds_sync();
+        select_top<kSurvivors / 64>(k2, p2, (ns + 63) / 64, R, s_sel, lane);
+        filtered = true;
       }
     }
   }
-  int n2 = 2;
-  while (n2 < R) n2 <<= 1;
-  for (int p = R + lane; p < n2; p += 64) s_sel[p] = 0ull;
-  wave_lds_sync();
-
-  // ---- bitonic sort, descending -------------------------------------------
-  for (int size = 2; size <= n2; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = lane; i < (n2 >> 1); i += 64) {
-        const int lo = 2 * stride * (i / stride) + (i % stride);
-        const int hi = lo + stride;
-        const uint64_t x = s_sel[lo], y = s_sel[hi];
-        const bool desc = (lo & size) == 0;
-        if (desc ? (x < y) : (x > y)) {
-          s_sel[lo] = y;
-          s_sel[hi] = x;
+  if (!filtered) {
+    uint32_t pos[kMaxSlots];
+#pragma unroll
+    for (int sl = 0; sl < kMaxSlots; ++sl) pos[sl] = (uint32_t)(64 * sl + lane);
+    select_top<kMaxSlots>(keys, pos, nslots, R, s_sel, lane);
+  }
+  if (R <= 128) {
+    // ---- rank each of the R survivors (2 per lane) by counting larger
+    // (key, ~index) pairs broadcast with readlane, then scatter into order
+    wave_lds_sync();
+    const uint64_t e0 = (lane < R) ? s_sel[lane] : 0ull;
+    const uint64_t e1 = (64 + lane < R) ? s_sel[64 + lane] : 0ull;
+    int r0 = 0, r1 = 0;
+    for (int j = 0; j < R; ++j) {
+      const uint64_t src = (j < 64) ? e0 : e1;     // j is wave-uniform
+      const int jl = j & 63;
+      const uint64_t x = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(src >> 32), jl) << 32) |
+                         (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)src, jl);
+      r0 += (x > e0) ? 1 : 0;
+      r1 += (x > e1) ? 1 : 0;
+    }
+    wave_lds_sync();
+    if (lane < R) s_sel[r0] = e0;
+    if (64 + lane < R) s_sel[r1] = e1;
+    wave_lds_sync();
+  } else {
+    int n2 = 2;
+    while (n2 < R) n2 <<= 1;
+    for (int p = R + lane; p < n2; p += 64) s_sel[p] = 0ull;
+    wave_lds_sync();
+    // ---- bitonic sort, descending -----------------------------------------
+    for (int size = 2; size <= n2; size <<= 1) {
+      for (int stride = size >> 1; stride > 0; stride >>= 1) {
+        for (int i = lane; i < (n2 >> 1); i += 64) {
+          const int lo = 2 * stride * (i / stride) + (i % stride);
+          const int hi = lo + stride;
+          const uint64_t x = s_sel[lo], y = s_sel[hi];
+          const bool desc = (lo & size) == 0;
+          if (desc ? (x < y) : (x > y)) {
+            s_sel[lo] = y;
+            s_sel[hi] = x;
+          }
         }
+        wave_lds_sync();
       }
-      wave_lds_sync();
     }
   }
 
@@ -428,7 +538,8 @@ hipError_t launch_score_select(const Shape& s, const uint16_t* Q, const uint16_t
   while (cap < rmax) cap <<= 1;
   P.sel_cap = cap;
   const int key_bytes = ((s.NB * 4 + 15) & ~15);
-  const int sel_bytes = 8 * cap;
+  int sel_bytes = 8 * cap;
+  if (sel_bytes < 8 * kSurvivors) sel_bytes = 8 * kSurvivors;
   P.wave_lds = key_bytes > sel_bytes ? key_bytes : sel_bytes;
   P.ring_lds = 0;
   if (s.d == 128)
