@@ -30,6 +30,7 @@
 //                 (16 lanes fetch a 4-key x 16-channel patch and each lane
 //                 receives the 4 keys of one channel).
 // Per listed block and unit: 4*64*64*d FLOP on 2*64*d*2 bytes of K/V.
+#include <atomic>
 #include <type_traits>
 
 #include "ugbs_internal.h"
@@ -50,6 +51,7 @@ struct AttnParams {
   uint16_t* O;
   int kv_width;
   int n_units;
+  int conc;          // units resident at once on one XCD (rotation period)
   float scale_log2;
 };
 
@@ -157,7 +159,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
   __shared__ __align__(16) uint16_t s_v[L::kElems];
   extern __shared__ int32_t s_list[];          // [kv_width]: at most kv_width distinct blocks
   __shared__ uint32_t s_bits[UGBS_MAX_BLOCKS / 32];
-  __shared__ int s_n;
+  __shared__ int s_n, s_below;
 
   const Shape& s = P.s;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -171,9 +173,17 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
 
   // ---- the tile's kept blocks, ascending (wave 0): kv_idx entries outside
   // 0..t are dropped and repeated entries count once (set semantics, as in
-  // Eq. (Attn)); ascending order puts the diagonal block t last (the only one
-  // needing the causal mask) and lets units that run side by side on an XCD
-  // sweep the key range together, so blocks they share are L2 hits.
+  // Eq. (Attn)), so the diagonal block t, the only one needing the causal
+  // mask, is the last entry when present.
+  //
+  // Visiting order.  The j-th workgroup an XCD receives starts its walk at
+  // the first listed block >= (j mod conc) / conc of its key range and wraps
+  // around (the diagonal block stays last).  Workgroups follow each other on
+  // an XCD in the order of j, conc of them at a time, so the ones resident
+  // together sweep the key range in step and blocks they share stay in that
+  // XCD's L2.  The order changes only the summation order of the softmax.
+  const int j_xcd = blockIdx.x >> 3;
+  const int start_blk = (int)(((long long)(j_xcd % P.conc) * u.t) / P.conc);
   if (w == 0) {
     const int32_t* kr = P.kv_idx + rowid * P.kv_width;
     const int nwords = (u.t >> 5) + 1;                 // bitmap words covering blocks 0..t
@@ -188,18 +198,34 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_wave_barrier();
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    int n = 0;
+    int n = 0, below = 0;
     for (int base = 0; base <= u.t; base += 64) {
       const int blk = base + lane;
       const bool on = blk <= u.t && ((s_bits[blk >> 5] >> (blk & 31)) & 1u);
       const uint64_t m = __ballot(on);
       if (on) s_list[n + __popcll(m & lt)] = blk;
       n += __popcll(m);
+      below += __popcll(__ballot(on && blk < start_blk));
     }
-    if (lane == 0) s_n = n;
+    if (lane == 0) {
+      s_n = n;
+      s_below = below;
+    }
   }
   __syncthreads();
-  const int n = s_n;
+  const int n = __builtin_amdgcn_readfirstlane(s_n);
+  const bool diag_last = n > 0 && s_list[n - 1] == u.t;
+  // entries 0..n_rot-1 are visited from position rot0 on, cyclically
+  const int n_rot = __builtin_amdgcn_readfirstlane(diag_last ? n - 1 : n);
+  const int rot0 = __builtin_amdgcn_readfirstlane(s_below < n_rot ? s_below : 0);
+  auto listed = [&](int i) {
+    int p = i;
+    if (i < n_rot) {
+      p = i + rot0;
+      if (p >= n_rot) p -= n_rot;
+    }
+    return __builtin_amdgcn_readfirstlane(s_list[p]);
+  };
 
   const size_t qo_base = ((size_t)u.b * s.H + u.h) * s.N + (size_t)u.t * kBlock;
   if (n == 0) {  // no attended key: O = 0
@@ -256,7 +282,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
   //   S(i+1) on the matrix cores overlaps the softmax of S(i) on the VALU,
   //   then O += P(i) V(i).  K(i+2) is fetched once S(i+1) is done, V(i+1)
   //   once PV(i) is done.  Fetch order per wave: K0 V0 K1 | K2 V1 | K3 V2 ...
-  int blk = __builtin_amdgcn_readfirstlane(s_list[0]);
+  int blk = listed(0);
   plan.fetch(Kh + (size_t)blk * Tile<D>::kElems, k_lds, w);
   plan.fetch(Vh + (size_t)blk * Tile<D>::kElems, v_lds, w);
   f32x4 sc[4][2];
@@ -265,7 +291,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
   compute_s(sc);
   wait_lgkm0();
   lds_barrier();                         // both waves are done reading s_k
-  if (n > 1) plan.fetch(Kh + (size_t)__builtin_amdgcn_readfirstlane(s_list[1]) * Tile<D>::kElems, k_lds, w);
+  if (n > 1) plan.fetch(Kh + (size_t)listed(1) * Tile<D>::kElems, k_lds, w);
 
   // One pipeline step for listed block `it`; MASK: it is the diagonal block
   // (always the last one), whose keys after the query row are masked.
@@ -273,7 +299,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
     constexpr bool MASK = decltype(mask_tag)::value;
     const bool has_next = it + 1 < n;
     const bool has_next2 = it + 2 < n;
-    const int nblk = has_next ? __builtin_amdgcn_readfirstlane(s_list[it + 1]) : 0;
+    const int nblk = has_next ? listed(it + 1) : 0;
 
     if (has_next) {                      // K(it+1) landed (V(it) may be in flight)
       if (it == 0) wait_vmcnt<0>(); else wait_vmcnt<NW>();
@@ -346,7 +372,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
       wait_lgkm0();
       lds_barrier();                     // both waves are done reading s_k
       if (has_next2)
-        plan.fetch(Kh + (size_t)__builtin_amdgcn_readfirstlane(s_list[it + 2]) * Tile<D>::kElems, k_lds, w);
+        plan.fetch(Kh + (size_t)listed(it + 2) * Tile<D>::kElems, k_lds, w);
     }
 
     // V(it) landed (K(it+2) may still be in flight)
@@ -394,7 +420,6 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
       for (int rt = 0; rt < 2; ++rt) sc[kt][rt] = sn[kt][rt];
   };
 
-  const bool diag_last = s_list[n - 1] == u.t;
   for (int it = 0; it + 1 < n; ++it) step(it, std::false_type{});
   if (diag_last) step(n - 1, std::true_type{});
   else step(n - 1, std::false_type{});
@@ -417,10 +442,33 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
   }
 }
 
+// Workgroups of attend_kernel<D> resident at once on one XCD, for the given
+// dynamic LDS size (occupancy per CU x CUs per XCD).  Cached per device as
+// one packed word (smem << 32 | value); a stale or missing entry only costs
+// a recomputation.  The value steers the visiting order, never the result.
+constexpr int kMaxDevices = 64;
 template <int D>
-hipError_t launch_t(const AttnParams& P, hipStream_t stream) {
+int xcd_concurrency(size_t smem) {
+  static std::atomic<uint64_t> cache[kMaxDevices];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev >= kMaxDevices) dev = -1;
+  if (dev >= 0) {
+    const uint64_t e = cache[dev].load(std::memory_order_relaxed);
+    if (e != 0 && (e >> 32) == (uint64_t)smem) return (int)(uint32_t)e;
+  }
+  int per_cu = 0, n_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attend_kernel<D>, 128, smem) != hipSuccess) per_cu = 1;
+  if (dev < 0 || hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) n_cu = 8;
+  const int conc = per_cu * n_cu / 8 > 0 ? per_cu * n_cu / 8 : 1;
+  if (dev >= 0) cache[dev].store(((uint64_t)smem << 32) | (uint32_t)conc, std::memory_order_relaxed);
+  return conc;
+}
+
+template <int D>
+hipError_t launch_t(AttnParams P, hipStream_t stream) {
   const size_t smem = sizeof(int32_t) * (size_t)P.kv_width;
   const int grid = ((P.n_units + 7) / 8) * 8;
+  P.conc = xcd_concurrency<D>(smem);
   attend_kernel<D><<<grid, 128, smem, stream>>>(P);
   return hipGetLastError();
 }
