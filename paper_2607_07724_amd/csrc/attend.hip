@@ -7,12 +7,14 @@
 //
 // Staging.  K and V blocks (64 keys x d, bf16) go global -> LDS with
 // direct-to-LDS loads (global_load_lds_dwordx4: no registers, no VALU).
-// Both live unpadded in natural [key][d] layout with the 16-byte column c of
-// row r stored at column c ^ (r mod d/8), which makes the MFMA operand reads
-// below bank-conflict free or nearly so.  K and V have one buffer each and
-// are refilled in a split ping-pong: K(i+1) is fetched as soon as both waves
-// have finished S(i), V(i+1) as soon as both have finished PV(i), so the
-// fetches overlap the softmax and the other matrix product.
+// Both live unpadded in natural [key][d] layout with the 16-byte columns of
+// each row permuted by an XOR swizzle (column c of row r of K at c ^ (r mod
+// d/8), of V at c ^ (2r mod d/8)), chosen so that the K-operand reads and the
+// transposing V reads below are free of LDS bank conflicts.  K and V have one
+// buffer each and are refilled in a split ping-pong: K(i+1) is fetched as
+// soon as both waves have finished S(i), V(i+1) as soon as both have
+// finished PV(i), so the fetches overlap the softmax and the other matrix
+// product.
 //
 // Compute, per block and wave (v_mfma_f32_16x16x32_bf16):
 //   S^T = K Q^T   K rows from LDS (ds_read_b128) are the A operand; the
@@ -102,8 +104,13 @@ struct Tile {
   static constexpr int kElems = kBlock * D;         // one K or V block
   static constexpr int kLoads = kBlock * CPR / 64;  // direct loads per block (64 chunks each)
   static constexpr int kLoadsPerWave = kLoads / 2;
-  // element offset of 16-byte column c of row r in the swizzled tile
-  __device__ static __forceinline__ int off(int r, int c) { return (r * CPR + (c ^ (r & (CPR - 1)))) * 8; }
+  static constexpr int kRowsPerLoad = 64 / CPR;
+  // Element offset of 16-byte column c of row r.  K: column c ^ (r mod CPR),
+  // so the 16 rows read by one K-operand load hit 16 different columns.
+  // V: column c ^ (2r mod CPR), so the 4-row x 2-column patches read by the
+  // transposing loads of one 16-lane group hit 8 different columns.
+  __device__ static __forceinline__ int swz(int r, bool v) { return (v ? 2 * r : r) & (CPR - 1); }
+  __device__ static __forceinline__ int off(int r, int c, bool v) { return (r * CPR + (c ^ swz(r, v))) * 8; }
 };
 
 // One direct-to-LDS 16-byte load per lane from base + voff (base is
@@ -125,27 +132,33 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const LDS_AS void*)p;
 }
 
-// Byte offsets (within a block) of the chunks this lane moves: fixed for the
-// whole kernel, so they are computed once.
-template <int D>
+// Direct-load plan of one K or V tile.  Load `inst` (0..kLoads-1) moves key
+// rows inst*R .. inst*R+R-1 (R = kRowsPerLoad) into LDS bytes inst*1024 ..
+// +1023, lane l writing LDS chunk inst*64+l, which holds global chunk
+// (l mod CPR) ^ swizzle(row).  The swizzle depends on the load index only
+// through inst mod M, so each lane keeps M byte offsets (row within the load
+// and column), and the rows of the load are added to the wave-uniform base.
+template <int D, bool V>
 struct FetchPlan {
-  uint32_t voff[Tile<D>::kLoadsPerWave];
-  __device__ __forceinline__ void init(int w, int lane) {
-    using L = Tile<D>;
+  using L = Tile<D>;
+  static constexpr int M = V ? (L::CPR > 2 * L::kRowsPerLoad ? L::CPR / (2 * L::kRowsPerLoad) : 1)
+                             : (L::CPR > L::kRowsPerLoad ? L::CPR / L::kRowsPerLoad : 1);
+  static_assert(L::kLoadsPerWave % M == 0, "wave's first load must be a multiple of M");
+  uint32_t voff[M];
+  __device__ __forceinline__ void init(int lane) {
 #pragma unroll
-    for (int i = 0; i < L::kLoadsPerWave; ++i) {
-      const int inst = w * L::kLoadsPerWave + i;
-      const int p = inst * 64 + lane;                  // LDS chunk written by this lane
-      const int r = p / L::CPR;
-      const int c = (p % L::CPR) ^ (r & (L::CPR - 1));  // global chunk that belongs there
-      voff[i] = (uint32_t)((r * D + c * 8) * 2);
+    for (int m = 0; m < M; ++m) {
+      const int r = m * L::kRowsPerLoad + lane / L::CPR;
+      const int c = (lane % L::CPR) ^ L::swz(r, V);
+      voff[m] = (uint32_t)(((lane / L::CPR) * D + c * 8) * 2);
     }
   }
   __device__ __forceinline__ void fetch(const uint16_t* src_blk, uint32_t tile_lds, int w) const {
-    using L = Tile<D>;
 #pragma unroll
-    for (int i = 0; i < L::kLoadsPerWave; ++i)
-      dma16(src_blk, voff[i], tile_lds + (uint32_t)((w * L::kLoadsPerWave + i) * 64 * 16));
+    for (int i = 0; i < L::kLoadsPerWave; ++i) {
+      const int inst = w * L::kLoadsPerWave + i;
+      dma16(src_blk + (size_t)inst * L::kRowsPerLoad * D, voff[i % M], tile_lds + (uint32_t)(inst * 64 * 16));
+    }
   }
 };
 
@@ -246,8 +259,10 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
 
   const uint16_t* Kh = P.K + ((size_t)u.b * s.Hkv + kvh) * s.N * D;
   const uint16_t* Vh = P.V + ((size_t)u.b * s.Hkv + kvh) * s.N * D;
-  FetchPlan<D> plan;
-  plan.init(w, lane);
+  FetchPlan<D, false> kplan;
+  FetchPlan<D, true> vplan;
+  kplan.init(lane);
+  vplan.init(lane);
   const uint32_t k_lds = __builtin_amdgcn_readfirstlane(lds_addr(s_k));
   const uint32_t v_lds = __builtin_amdgcn_readfirstlane(lds_addr(s_v));
 
@@ -270,7 +285,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
         const int r = 16 * kt + c16;
-        const bf16x8 ak = as_bf16x8(*reinterpret_cast<const uint4*>(s_k + L::off(r, 4 * ks + g)));
+        const bf16x8 ak = as_bf16x8(*reinterpret_cast<const uint4*>(s_k + L::off(r, 4 * ks + g, false)));
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
           sc[kt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, bq[rt][ks], sc[kt][rt], 0, 0, 0);
@@ -283,15 +298,15 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
   //   then O += P(i) V(i).  K(i+2) is fetched once S(i+1) is done, V(i+1)
   //   once PV(i) is done.  Fetch order per wave: K0 V0 K1 | K2 V1 | K3 V2 ...
   int blk = listed(0);
-  plan.fetch(Kh + (size_t)blk * Tile<D>::kElems, k_lds, w);
-  plan.fetch(Vh + (size_t)blk * Tile<D>::kElems, v_lds, w);
+  kplan.fetch(Kh + (size_t)blk * Tile<D>::kElems, k_lds, w);
+  vplan.fetch(Vh + (size_t)blk * Tile<D>::kElems, v_lds, w);
   f32x4 sc[4][2];
   wait_vmcnt<NW>();                      // K0 landed
   lds_barrier();
   compute_s(sc);
   wait_lgkm0();
   lds_barrier();                         // both waves are done reading s_k
-  if (n > 1) plan.fetch(Kh + (size_t)listed(1) * Tile<D>::kElems, k_lds, w);
+  if (n > 1) kplan.fetch(Kh + (size_t)listed(1) * Tile<D>::kElems, k_lds, w);
 
   // One pipeline step for listed block `it`; MASK: it is the diagonal block
   // (always the last one), whose keys after the query row are masked.
@@ -372,7 +387,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
       wait_lgkm0();
       lds_barrier();                     // both waves are done reading s_k
       if (has_next2)
-        plan.fetch(Kh + (size_t)listed(it + 2) * Tile<D>::kElems, k_lds, w);
+        kplan.fetch(Kh + (size_t)listed(it + 2) * Tile<D>::kElems, k_lds, w);
     }
 
     // V(it) landed (K(it+2) may still be in flight)
@@ -399,9 +414,9 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
         const int r0 = 32 * j + tr_row, r1 = r0 + 16;
         const int c = 2 * dt + tr_col;
         const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (LDS_AS v4i16*)(s_v + L::off(r0, c) + tr_half));
+            (LDS_AS v4i16*)(s_v + L::off(r0, c, true) + tr_half));
         const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (LDS_AS v4i16*)(s_v + L::off(r1, c) + tr_half));
+            (LDS_AS v4i16*)(s_v + L::off(r1, c, true) + tr_half));
         const bf16x8 av = __builtin_bit_cast(
             bf16x8, (short __attribute__((ext_vector_type(8)))){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
 #pragma unroll
@@ -413,7 +428,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
     wait_lgkm0();
     lds_barrier();                       // both waves are done reading s_v
-    if (has_next) plan.fetch(Vh + (size_t)nblk * Tile<D>::kElems, v_lds, w);
+    if (has_next) vplan.fetch(Vh + (size_t)nblk * Tile<D>::kElems, v_lds, w);
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
