@@ -322,6 +322,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
     // S(it+1): on the last block this re-reads s_k (no fetch is pending) and is discarded
     f32x4 sn[4][2];
+    __builtin_amdgcn_s_setprio(1);       // matrix-core phases issue ahead of other waves' fetch phases
     compute_s(sn);
 
     // online softmax of S(it) (base 2); lane holds row (32w + 16rt + c16),
@@ -383,6 +384,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
       }
     }
 
+    __builtin_amdgcn_s_setprio(0);
     if (has_next) {
       wait_lgkm0();
       lds_barrier();                     // both waves are done reading s_k
@@ -394,6 +396,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
     if (has_next2) wait_vmcnt<NW>(); else wait_vmcnt<0>();
     lds_barrier();
 
+    __builtin_amdgcn_s_setprio(1);
     if (__ballot(moved)) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
@@ -426,6 +429,7 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
         }
       }
     }
+    __builtin_amdgcn_s_setprio(0);
     wait_lgkm0();
     lds_barrier();                       // both waves are done reading s_v
     if (has_next) vplan.fetch(Vh + (size_t)nblk * Tile<D>::kElems, v_lds, w);
