@@ -42,6 +42,10 @@ def parse():
     ap.add_argument("--json-out", default=None)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain streaming kernel (1 GiB in, 1 GiB out) to scale HBM counters")
+    ap.add_argument("--no-probe", action="store_true", help="skip the measured copy / GEMM peaks")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache steps")
+    ap.add_argument("--stack", action="store_true",
+                    help="also time the 28-layer 128K stack (28/4 heads, both backbones) routed vs dense")
     return ap.parse_args()
 
 
@@ -157,7 +161,27 @@ def main():
     ms_per_step = 1e3 * wall / a.steps
     stage_ms = np.array([[evs[i][j].elapsed_time(evs[i][j + 1]) for j in range(4)] for i in range(a.steps)])
     stage_avg = stage_ms.mean(axis=0)
+    step_ms = np.array([evs[i][0].elapsed_time(evs[i][4]) for i in range(a.steps)])
     log(f"timed {a.steps} steps: {ms_per_step:.3f} ms/step; stages {np.round(stage_avg, 4).tolist()}")
+
+    cold = None
+    if not a.no_cold:
+        # caches cold: a 1 GiB write (twice the 256 MB last-level cache) before each single step
+        flush = torch.empty(1 << 28, dtype=torch.int32, device=dev)
+        cold_ms = []
+        for i in range(3):
+            flush.fill_(i)
+            torch.cuda.synchronize(dev)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+            step(ev)
+            torch.cuda.synchronize(dev)
+            cold_ms.append([ev[j].elapsed_time(ev[j + 1]) for j in range(4)])
+        del flush
+        cm = np.array(cold_ms)
+        cold = {"ms_median": round(float(np.median(cm.sum(axis=1))), 4),
+                "stages_ms_median": np.round(np.median(cm, axis=0), 4).tolist(),
+                "runs": 3, "flush": "1 GiB device write before each step"}
+        log(f"cold: {cold}")
 
     kv = bufs.kv_idx.cpu().numpy()
     trig = bufs.trigger.cpu().numpy()
@@ -241,6 +265,15 @@ def main():
         }
         log(f"dense: {dense}")
 
+    probe = None
+    if not a.no_probe:
+        probe = measured_peaks(torch, dev, stream)
+        log(f"measured peaks: {probe}")
+        roofline["measured_peak_TFLOPs"] = probe["gemm_bf16_TFLOPs"]
+        roofline["frac_of_measured_peak"] = round(roofline["achieved"] / probe["gemm_bf16_TFLOPs"], 4)
+
+    stack = run_stack(torch, dev, ugbs, synth, a.steps) if a.stack else None
+
     cpu = None
     if not a.no_cpu:
         cpu = cpu_baseline(w, inp, a.cpu_units)
@@ -273,6 +306,10 @@ def main():
         "selection": {"mean_kept_blocks": round(float(kept.mean()), 3),
                       "triggered_tiles": int(trig.sum()),
                       "needle_hit_rate": hit_rate},
+        "ms_per_step_median": round(float(np.median(step_ms)), 4),
+        "cold": cold,
+        "measured_peaks": probe,
+        "stack": stack,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
@@ -281,6 +318,107 @@ def main():
     if a.json_out:
         with open(a.json_out, "w") as f:
             f.write(line + "\n")
+
+
+def measured_peaks(torch, dev, stream):
+    """Practical ceilings measured on this GPU: a streaming elementwise add
+    (1 GiB read + 1 GiB written) and a large bf16 GEMM (8192^3)."""
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    src = torch.ones(1 << 29, dtype=torch.int16, device=dev)
+    dst = torch.empty_like(src)
+    torch.add(src, 1, out=dst)
+    torch.cuda.synchronize(dev)
+    e0.record(stream)
+    for _ in range(5):
+        torch.add(src, 1, out=dst)
+    e1.record(stream)
+    torch.cuda.synchronize(dev)
+    copy_gbps = 5 * 2 * (1 << 30) / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    n = 8192
+    A = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    B = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    C = A @ B
+    torch.cuda.synchronize(dev)
+    e0.record(stream)
+    for _ in range(10):
+        torch.matmul(A, B, out=C)
+    e1.record(stream)
+    torch.cuda.synchronize(dev)
+    gemm = 10 * 2.0 * n ** 3 / (e0.elapsed_time(e1) * 1e-3) / 1e12
+    del A, B, C
+    return {"copy_GBps": round(copy_gbps, 1), "gemm_bf16_TFLOPs": round(gemm, 1),
+            "copy": "torch elementwise add, 1 GiB in + 1 GiB out", "gemm": "torch.matmul bf16 8192^3"}
+
+
+def run_stack(torch, dev, ugbs, synth, steps):
+    """28-layer attention-only stack at the 28/4-head d 128 shape, N = 131072:
+    per-layer inputs (independent seeds) resident in HBM, per-layer quantile;
+    routed pipeline for both backbones vs dense causal attention, summed over
+    the layers."""
+    import torch.nn.functional as F
+    w0 = synth.WORKLOADS["C5"]
+    L = w0.layers
+    t0 = time.time()
+    layers = []
+    for layer in range(L):
+        inp = synth.generate(w0, layer=layer, threads=16)
+        cv = lambda x: torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+        layers.append((cv(inp.Q), cv(inp.K), cv(inp.V)))
+        del inp
+    log(f"stack: {L} layers generated and uploaded in {time.time() - t0:.1f}s")
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    out = {"layers": L, "workload": "C5: 28-layer stack, 28 q / 4 kv heads, d 128, N 131072, k 64, q 0.1"}
+    O = torch.empty_like(layers[0][0])
+    for name, bb in (("kmean", synth.KMEAN), ("quest", synth.QUEST)):
+        p = ugbs.Problem.make(w0.B, w0.H, w0.Hkv, w0.N, w0.d, w0.k, w0.q, bb)
+        bufs = ugbs.Buffers(p, device=dev)
+        for Q, K, V in layers[:2]:
+            ugbs.prefill(p, Q, K, V, O, bufs)
+        torch.cuda.synchronize(dev)
+        reps = max(1, min(steps, 3))
+        e0.record(stream)
+        for _ in range(reps):
+            for Q, K, V in layers:
+                ugbs.prefill(p, Q, K, V, O, bufs)
+        e1.record(stream)
+        torch.cuda.synchronize(dev)
+        ms = e0.elapsed_time(e1) / reps
+        out[name] = {"routed_ms": round(ms, 2), "per_layer_ms": round(ms / L, 3)}
+        del bufs
+    G = w0.H // w0.Hkv
+    try:
+        from torch.nn.attention import SDPBackend, sdpa_kernel
+        # GQA heads expanded for SDPA outside the timed region (as in the single-layer leg)
+        expanded = [(K.repeat_interleave(G, dim=1), V.repeat_interleave(G, dim=1)) for _, K, V in layers]
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
+            F.scaled_dot_product_attention(layers[0][0], *expanded[0], is_causal=True)
+            torch.cuda.synchronize(dev)
+            e0.record(stream)
+            for (Q, _, _), (Ke, Ve) in zip(layers, expanded):
+                F.scaled_dot_product_attention(Q, Ke, Ve, is_causal=True)
+            e1.record(stream)
+            torch.cuda.synchronize(dev)
+        del expanded
+        sd = e0.elapsed_time(e1)
+        out["dense_sdpa_ms"] = round(sd, 1)
+        for name in ("kmean", "quest"):
+            out[name]["routed_over_sdpa"] = round(out[name]["routed_ms"] / sd, 4)
+    except Exception as ex:
+        log(f"stack SDPA failed: {ex!r}")
+    kvd = torch.from_numpy(synth.dense_kv_idx(w0.B, w0.H, w0.T)).to(dev)
+    pd = ugbs.Problem.make(w0.B, w0.H, w0.Hkv, w0.N, w0.d, w0.NB, 0.0, w0.backbone)
+    e0.record(stream)
+    for Q, K, V in layers:
+        ugbs.ugbs_attend(pd, Q, K, V, kvd, O)
+    e1.record(stream)
+    torch.cuda.synchronize(dev)
+    out["dense_ugbs_ms"] = round(e0.elapsed_time(e1), 1)
+    del layers, O, kvd
+    torch.cuda.empty_cache()
+    log(f"stack: {out}")
+    return out
 
 
 def cpu_baseline(w, inp, n_units):
