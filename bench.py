@@ -135,7 +135,7 @@ def main():
         ugbs.ugbs_block_meta(p, K, bufs.meta)
         if ev is not None:
             ev[1].record(stream)
-        ugbs.ugbs_score_select(p, Q, bufs.meta, bufs.idx_sorted, bufs.sigma)
+        ugbs.ugbs_score_select(p, Q, bufs.meta, bufs.idx_sorted, bufs.sigma, workspace=bufs.workspace)
         if ev is not None:
             ev[2].record(stream)
         ugbs.ugbs_route(p, bufs.sigma, bufs.idx_sorted, bufs.kv_idx, bufs.workspace,

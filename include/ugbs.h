@@ -13,7 +13,7 @@
  *
  * Pipeline for one layer, four stream-ordered calls:
  *   ugbs_block_meta   (K)                    -> meta
- *   ugbs_score_select (Q, meta)              -> idx_sorted, sigma
+ *   ugbs_score_select (Q, meta, workspace)   -> idx_sorted, sigma
  *   ugbs_route        (sigma, idx_sorted)    -> kv_idx (may alias idx_sorted)
  *   ugbs_attend       (Q, K, V, kv_idx)      -> O
  * No call synchronises the device; none allocates device memory.
@@ -51,7 +51,7 @@ extern "C" {
 #define UGBS_API
 #endif
 
-#define UGBS_ABI_VERSION 1
+#define UGBS_ABI_VERSION 2
 #define UGBS_BLOCK 64          /* BLOCK_M = BLOCK_N = 64 tokens (Section 3.1, 3.2) */
 #define UGBS_MAX_BLOCKS 2048   /* N_B <= 2048, i.e. N <= 131072 */
 #define UGBS_MAX_KV_WIDTH 4096 /* kv_width accepted by ugbs_attend; k_budget <= 2048 */
@@ -124,10 +124,17 @@ UGBS_API int ugbs_block_meta(const ugbs_problem* p, const void* K, void* meta, v
  *                candidate scores c (fp32 arithmetic), 0 when the
  *                denominator is 0, and -1 when |C(t)| <= m (a saturated
  *                tile: it keeps every visible block).
+ *   workspace  : needed only when scores_in and scores_out are both NULL
+ *                (the tile scores then pass through it): device memory of
+ *                at least ugbs_workspace_bytes(p) bytes, 256-byte aligned,
+ *                owned by the caller, contents on entry ignored; otherwise
+ *                may be NULL.  Two calls that overlap in time must not share
+ *                a workspace.
  *   Q and meta are read-only; idx_sorted/sigma/scores_out are fully written. */
 UGBS_API int ugbs_score_select(const ugbs_problem* p, const void* Q, const void* meta,
                       const float* scores_in, float* scores_out,
-                      int32_t* idx_sorted, float* sigma, void* stream);
+                      int32_t* idx_sorted, float* sigma,
+                      void* workspace, size_t workspace_bytes, void* stream);
 
 /* Stage 4 -- head mean, per-layer quantile trigger and padded expansion
  * (A.7-A.9; Eq. (trigger)).
@@ -171,7 +178,10 @@ UGBS_API int ugbs_route(const ugbs_problem* p, const float* sigma, const int32_t
 UGBS_API int ugbs_attend(const ugbs_problem* p, const void* Q, const void* K, const void* V,
                 const int32_t* kv_idx, int32_t kv_width, void* O, void* stream);
 
-/* Bytes of device workspace ugbs_route needs for problem p (0 if p is invalid). */
+/* Bytes of device workspace ugbs_score_select (without scores_in/scores_out)
+ * and ugbs_route need for problem p; one workspace serves both calls in
+ * sequence on a stream (0 if p is invalid).  For the score pass it holds
+ * B H (T-1)(T-2)/2 fp32 candidate scores. */
 UGBS_API size_t ugbs_workspace_bytes(const ugbs_problem* p);
 
 /* Static, human-readable text for a ugbs_status value. */

@@ -96,7 +96,7 @@ def lib():
         P = ctypes.c_void_p
         pp = ctypes.POINTER(Problem)
         L.ugbs_block_meta.argtypes = [pp, P, P, P]
-        L.ugbs_score_select.argtypes = [pp, P, P, P, P, P, P, P]
+        L.ugbs_score_select.argtypes = [pp, P, P, P, P, P, P, P, ctypes.c_size_t, P]
         L.ugbs_route.argtypes = [pp, P, P, P, P, P, P, P, ctypes.c_size_t, P]
         L.ugbs_attend.argtypes = [pp, P, P, P, P, ctypes.c_int32, P, P]
         L.ugbs_workspace_bytes.argtypes = [pp]
@@ -172,8 +172,10 @@ def ugbs_block_meta(p: Problem, K, meta, stream=None):
 
 
 def ugbs_score_select(p: Problem, Q, meta, idx_sorted, sigma, scores_in=None, scores_out=None,
-                      stream=None):
-    """Stages 2-3 (A.2-A.6): -> idx_sorted [B,H,T,2k] int32, sigma [B,H,T] fp32."""
+                      stream=None, workspace=None):
+    """Stages 2-3 (A.2-A.6): -> idx_sorted [B,H,T,2k] int32, sigma [B,H,T] fp32.
+    Without scores_in/scores_out the tile scores pass through `workspace`
+    (>= ugbs_workspace_bytes(p) bytes)."""
     import torch
     bf = _bf16()
     dev = Q.device
@@ -183,8 +185,12 @@ def ugbs_score_select(p: Problem, Q, meta, idx_sorted, sigma, scores_in=None, sc
     so = _opt("scores_out", scores_out, (p.batch, p.n_heads, p.T, p.NB), (torch.float32,), dev)
     ix = _check("idx_sorted", idx_sorted, (p.batch, p.n_heads, p.T, p.W), (torch.int32,), dev)
     sg = _check("sigma", sigma, (p.batch, p.n_heads, p.T), (torch.float32,), dev)
+    ws, nbytes = None, 0
+    if workspace is not None:
+        ws = _check("workspace", workspace, tuple(workspace.shape), (workspace.dtype,), dev)
+        nbytes = workspace.numel() * workspace.element_size()
     _raise("ugbs_score_select",
-           lib().ugbs_score_select(ctypes.byref(p), q, m, si, so, ix, sg, _stream(stream)))
+           lib().ugbs_score_select(ctypes.byref(p), q, m, si, so, ix, sg, ws, nbytes, _stream(stream)))
 
 
 def ugbs_route(p: Problem, sigma, idx_sorted, kv_idx, workspace, sigma_bar=None, tau=None,
@@ -245,7 +251,8 @@ class Buffers:
 def prefill(p: Problem, Q, K, V, O, bufs: Buffers, stream=None, scores_in=None, scores_out=None):
     """Run the four stages in order on one stream: meta, score+select, route, attend."""
     ugbs_block_meta(p, K, bufs.meta, stream)
-    ugbs_score_select(p, Q, bufs.meta, bufs.idx_sorted, bufs.sigma, scores_in, scores_out, stream)
+    ugbs_score_select(p, Q, bufs.meta, bufs.idx_sorted, bufs.sigma, scores_in, scores_out, stream,
+                      workspace=bufs.workspace)
     ugbs_route(p, bufs.sigma, bufs.idx_sorted, bufs.kv_idx, bufs.workspace, bufs.sigma_bar,
                bufs.tau, bufs.trigger, stream)
     ugbs_attend(p, Q, K, V, bufs.kv_idx, O, stream)

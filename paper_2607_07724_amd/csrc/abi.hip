@@ -97,17 +97,20 @@ int ugbs_block_meta(const ugbs_problem* p, const void* K, void* meta, void* stre
 
 int ugbs_score_select(const ugbs_problem* p, const void* Q, const void* meta,
                       const float* scores_in, float* scores_out, int32_t* idx_sorted,
-                      float* sigma, void* stream) {
+                      float* sigma, void* workspace, size_t workspace_bytes, void* stream) {
   Shape s;
   int st = make_shape(p, &s);
   if (st) return st;
   if (!Q || !meta || !idx_sorted || !sigma) return UGBS_ERR_NULL;
+  const bool needs_ws = !scores_in && !scores_out;
+  if (needs_ws && (!workspace || workspace_bytes < ugbs::ws_total(s))) return UGBS_ERR_WORKSPACE;
   if (!aligned(Q, 16) || !aligned(meta, 16) || !aligned(idx_sorted, 4) || !aligned(sigma, 4) ||
-      !aligned(scores_in, 4) || !aligned(scores_out, 4))
+      !aligned(scores_in, 4) || !aligned(scores_out, 4) || (needs_ws && !aligned(workspace, 256)))
     return UGBS_ERR_ALIGN;
   return hip_status(ugbs::launch_score_select(
       s, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(meta), scores_in,
-      scores_out, idx_sorted, sigma, static_cast<hipStream_t>(stream)));
+      scores_out, idx_sorted, sigma, needs_ws ? workspace : nullptr,
+      static_cast<hipStream_t>(stream)));
 }
 
 int ugbs_route(const ugbs_problem* p, const float* sigma, const int32_t* idx_sorted,

@@ -1,10 +1,10 @@
 // Stages 2+3: tile scores, forcing, sorted top-2k and the cutoff margin
-// (A.2-A.6; Eqs. (tile-score), (sigma-def)).
+// (A.2-A.6; Eqs. (tile-score), (sigma-def)).  Two kernels on one stream.
 //
-// One workgroup per (batch, kv head, Q-tile, group of up to 4 sibling query
-// heads); each wave owns one query head's unit (64 rows of tile t).
-//
-// Scoring is a dense contraction on bf16 MFMA (v_mfma_f32_16x16x32_bf16):
+// score_kernel: one workgroup per (batch, kv head, Q-tile, group of up to 4
+// sibling query heads); each wave owns one query head's unit (64 rows of
+// tile t).  Scoring is a dense contraction on bf16 MFMA
+// (v_mfma_f32_16x16x32_bf16):
 //   S[64 rows x 16 blocks] = Qx[64 x KD] * Mx[KD x 16 blocks]
 // with, for K-mean, Qx = Q and Mx = kbar (KD = d), and for Quest the exact
 // split form of Eq. (quest-score): for kmax >= kmin,
@@ -18,24 +18,28 @@
 // the 16-byte column c of row r sits at c ^ (r mod 16), which makes the
 // operand reads bank-conflict free.  The max over the tile's rows (A.3) is
 // the max over a lane's 16 accumulators and then across the four 16-lane
-// groups.
+// groups; the 16 tile scores of a chunk go to memory as one 64-byte store,
+// into the caller's [.., N_B] score tensor or into packed rows of the
+// workspace (row (b, h, t) holds the t-1 candidates 1..t-1).
 //
-// Selection (per wave, no workgroup barriers): tile scores become
-// order-preserving 32-bit keys (-0 folded into +0).  A per-lane top-2
-// pre-filter bounds the R-th largest key from below (R = min(2k - |F|, |C|)),
-// the R-th largest key is found among the survivors by a
+// select_kernel: one wave per unit, heaviest tile first.  Tile scores
+// become order-preserving 32-bit keys (-0 folded into +0).  A per-lane
+// top-2 pre-filter bounds the R-th largest key from below (R = min(2k -
+// |F|, |C|)), the R-th largest key is found among the survivors by a
 // most-significant-bit-first radix descent that counts with wave ballots,
 // the top R are compacted (equal keys at the threshold by lower block
 // index) and ordered by (key, ~index): for R <= 128 each survivor's rank is
 // counted in registers from readlane broadcasts and it is scattered into
 // place, otherwise a bitonic sort in LDS.  sigma uses IEEE fp32 subtract and
-// divide.
+// divide.  Splitting the stages keeps each kernel at its own occupancy (the
+// scoring kernel is bound by registers, the selection kernel by latency).
 #include "ugbs_internal.h"
 
 namespace ugbs {
 namespace {
 
 constexpr int kMaxGroup = 4;    // sibling query heads per workgroup
+constexpr int kSelWaves = 4;    // units (waves) per selection workgroup
 constexpr int kRing = 4;        // metadata chunk slots (kRing - 1 in flight)
 constexpr int kChunk = 16;      // blocks per metadata chunk
 
@@ -49,13 +53,21 @@ struct SelParams {
   float* scores_out;
   int32_t* idx_sorted;
   float* sigma;
-  int GW;         // waves (query heads) per workgroup
+  float* scratch; // packed candidate scores (workspace), when neither scores_in nor scores_out
+  int GW;         // waves (query heads) per workgroup of the score kernel
   int n_groups;   // head groups per kv head = ceil(G / GW)
-  int n_wg;       // workgroups
-  int sel_cap;    // power of two >= max survivors
-  int wave_lds;   // bytes of per-wave LDS (keys, then survivors)
+  int n_wg;       // score-kernel workgroups
+  int wave_lds;   // bytes of per-wave LDS of the selection kernel (survivors)
   int ring_lds;   // bytes of the metadata ring
 };
+
+// Offset (floats) of the packed candidate row of unit (bh, t): rows of one
+// (b, h) follow each other, row t holding t-1 scores.
+__device__ __forceinline__ size_t packed_row(int bh, int t, int T) {
+  const size_t tri = (T >= 2) ? (size_t)(T - 1) * (T - 2) / 2 : 0;
+  const size_t off = (t >= 2) ? (size_t)(t - 1) * (t - 2) / 2 : 0;
+  return (size_t)bh * tri + off;
+}
 
 __device__ __forceinline__ uint32_t order_key(float f) {
   uint32_t u = __float_as_uint(f == 0.0f ? 0.0f : f);
@@ -233,8 +245,8 @@ __device__ __forceinline__ Group group_of(int id, const SelParams& P) {
   return r;
 }
 
-template <int D, bool QUEST>
-__global__ void __launch_bounds__(64 * kMaxGroup) score_select_kernel(SelParams P) {
+template <int D, bool QUEST, bool PACKED>
+__global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
   using MC = MetaChunk<D, QUEST>;
   constexpr int KD = MC::KD;
   constexpr int KS = KD / 32;
@@ -254,20 +266,12 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_select_kernel(SelParams 
   const size_t row = ((size_t)gr.b * s.H + h) * s.T + t;
   const int nf = (t == 0) ? 1 : 2;
   const int nc = (t >= 1) ? t - 1 : 0;
-  const int m = s.k - nf;
-  const int W = s.W;
-  const int R = min(W - nf, nc);
 
   unsigned char* ring = smem;
-  uint32_t* s_key = reinterpret_cast<uint32_t*>(smem + P.ring_lds + w * P.wave_lds);  // [NB]
-  uint64_t* s_sel = reinterpret_cast<uint64_t*>(s_key);  // reused after the keys are in registers
 
-  if (nc > 0 && P.scores_in) {
-    if (active) {
-      const float* src = P.scores_in + row * s.NB + 1;
-      for (int p = lane; p < nc; p += 64) s_key[p] = order_key(src[p]);
-    }
-  } else if (nc > 0) {
+  // this unit's candidate scores 1..nc: packed rows, or the full [.., N_B] row
+  float* dst = PACKED ? P.scratch + packed_row(gr.b * s.H + h, t, s.T) : P.scores_out + row * s.NB + 1;
+  if (nc > 0) {
     // ---- A operand: this wave's 64 query rows (Quest: [q- | q+]) ----------
     bf16x8 a[4][KS];
     const uint16_t* qtile = P.Q + (((size_t)gr.b * s.H + h) * s.N + (size_t)t * kBlock) * D;
@@ -349,18 +353,43 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_select_kernel(SelParams 
           for (int i = 0; i < 4; ++i) mx = fmaxf(mx, acc[rt][i]);
         mx = wave_max16(mx);
         const int pos = kChunk * c + c16;
-        if (g == 0 && pos < nc) s_key[pos] = order_key(mx);
+        if (g == 0 && pos < nc) dst[pos] = mx;
       }
     }
   }
-  if (!active) return;
-  wave_lds_sync();
+  if (!active || PACKED) return;
+  // full layout: -inf outside C(t) = {1..t-1}
+  float* full = P.scores_out + row * s.NB;
+  for (int p = lane; p < s.NB; p += 64)
+    if (p == 0 || p > nc) full[p] = -__builtin_huge_valf();
+}
 
-  if (P.scores_out) {
-    float* dst = P.scores_out + row * s.NB;
-    for (int p = lane; p < s.NB; p += 64)
-      dst[p] = (p >= 1 && p <= nc) ? key_value(s_key[p - 1]) : -__builtin_huge_valf();
-  }
+// One wave per (b, h, t) unit, heaviest tile first; reads the unit's
+// candidate scores (packed rows of the score kernel, or a full [.., N_B] row)
+template <bool PACKED>
+__global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const Shape& s = P.s;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int n_units = s.B * s.H * s.T;
+  const int n_wg = (n_units + kSelWaves - 1) / kSelWaves;
+  const int wg = xcd_remap(blockIdx.x, n_wg);
+  if (wg >= n_wg) return;
+  const int u = wg * kSelWaves + w;
+  if (u >= n_units) return;
+  const int h = u % s.H;
+  const int rest = u / s.H;
+  const int t = s.T - 1 - rest % s.T;
+  const int b = rest / s.T;
+  const size_t row = ((size_t)b * s.H + h) * s.T + t;
+  const int nf = (t == 0) ? 1 : 2;
+  const int nc = (t >= 1) ? t - 1 : 0;
+  const int m = s.k - nf;
+  const int W = s.W;
+  const int R = min(W - nf, nc);
+  uint64_t* s_sel = reinterpret_cast<uint64_t*>(smem + w * P.wave_lds);
+  const float* src = PACKED ? P.scratch + packed_row(b * s.H + h, t, s.T) : P.scores_in + row * s.NB + 1;
 
   int32_t* out = P.idx_sorted + row * W;
   if (nc == 0) {
@@ -381,9 +410,8 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_select_kernel(SelParams 
 #pragma unroll
   for (int sl = 0; sl < kMaxSlots; ++sl) {
     const int p = 64 * sl + lane;
-    keys[sl] = (sl < nslots && p < nc) ? s_key[p] : 0u;  // valid keys are >= 0x007fffff
+    keys[sl] = (sl < nslots && p < nc) ? order_key(src[p]) : 0u;  // valid keys are >= 0x007fffff
   }
-  wave_lds_sync();                                       // s_key is reused for survivors below
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   bool filtered = false;
   if (R <= 128 && nc > R) {
@@ -502,26 +530,52 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_select_kernel(SelParams 
   }
 }
 
-template <int D, bool QUEST>
-hipError_t launch_t(SelParams P, hipStream_t stream) {
+template <int D, bool QUEST, bool PACKED>
+hipError_t launch_score(SelParams P, hipStream_t stream) {
   using MC = MetaChunk<D, QUEST>;
   P.ring_lds = kRing * MC::kBytes;
-  const size_t smem = (size_t)P.ring_lds + (size_t)P.GW * P.wave_lds;
+  const size_t smem = (size_t)P.ring_lds;
+  const int grid = ((P.n_wg + 7) / 8) * 8;
+  score_kernel<D, QUEST, PACKED><<<grid, 64 * P.GW, smem, stream>>>(P);
+  return hipGetLastError();
+}
+
+template <bool PACKED>
+hipError_t launch_select(const SelParams& P, hipStream_t stream) {
+  const size_t smem = (size_t)kSelWaves * P.wave_lds;
   if (smem > 65536) {  // large budgets (k near N_B): raise the dynamic-LDS limit
-    const hipError_t e = hipFuncSetAttribute((const void*)score_select_kernel<D, QUEST>,
+    const hipError_t e = hipFuncSetAttribute((const void*)select_kernel<PACKED>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
   }
-  const int grid = ((P.n_wg + 7) / 8) * 8;
-  score_select_kernel<D, QUEST><<<grid, 64 * P.GW, smem, stream>>>(P);
+  const int n_units = P.s.B * P.s.H * P.s.T;
+  const int n_wg = (n_units + kSelWaves - 1) / kSelWaves;
+  const int grid = ((n_wg + 7) / 8) * 8;
+  select_kernel<PACKED><<<grid, 64 * kSelWaves, smem, stream>>>(P);
   return hipGetLastError();
+}
+
+template <bool PACKED>
+hipError_t launch_score_d(const SelParams& P, hipStream_t stream) {
+  const Shape& s = P.s;
+  if (s.d == 128)
+    return s.backbone == UGBS_QUEST ? launch_score<128, true, PACKED>(P, stream)
+                                    : launch_score<128, false, PACKED>(P, stream);
+  return s.backbone == UGBS_QUEST ? launch_score<64, true, PACKED>(P, stream)
+                                  : launch_score<64, false, PACKED>(P, stream);
 }
 
 }  // namespace
 
+size_t score_scratch_bytes(const Shape& s) {
+  const size_t tri = (s.T >= 2) ? (size_t)(s.T - 1) * (s.T - 2) / 2 : 0;
+  return sizeof(float) * (size_t)s.B * s.H * tri;
+}
+
 hipError_t launch_score_select(const Shape& s, const uint16_t* Q, const uint16_t* meta,
                                const float* scores_in, float* scores_out,
-                               int32_t* idx_sorted, float* sigma, hipStream_t stream) {
+                               int32_t* idx_sorted, float* sigma, void* workspace,
+                               hipStream_t stream) {
   SelParams P;
   P.s = s;
   P.Q = Q;
@@ -530,21 +584,27 @@ hipError_t launch_score_select(const Shape& s, const uint16_t* Q, const uint16_t
   P.scores_out = scores_out;
   P.idx_sorted = idx_sorted;
   P.sigma = sigma;
+  P.scratch = static_cast<float*>(workspace);
   P.GW = s.G < kMaxGroup ? s.G : kMaxGroup;
   P.n_groups = (s.G + P.GW - 1) / P.GW;
   P.n_wg = s.B * s.Hkv * s.T * P.n_groups;
   int cap = 2;
   const int rmax = s.W < s.NB ? s.W : s.NB;
   while (cap < rmax) cap <<= 1;
-  P.sel_cap = cap;
-  const int key_bytes = ((s.NB * 4 + 15) & ~15);
   int sel_bytes = 8 * cap;
   if (sel_bytes < 8 * kSurvivors) sel_bytes = 8 * kSurvivors;
-  P.wave_lds = key_bytes > sel_bytes ? key_bytes : sel_bytes;
+  P.wave_lds = sel_bytes;
   P.ring_lds = 0;
-  if (s.d == 128)
-    return s.backbone == UGBS_QUEST ? launch_t<128, true>(P, stream) : launch_t<128, false>(P, stream);
-  return s.backbone == UGBS_QUEST ? launch_t<64, true>(P, stream) : launch_t<64, false>(P, stream);
+  if (scores_in) return launch_select<false>(P, stream);
+  if (scores_out) {
+    const hipError_t e = launch_score_d<false>(P, stream);
+    if (e != hipSuccess) return e;
+    P.scores_in = scores_out;
+    return launch_select<false>(P, stream);
+  }
+  const hipError_t e = launch_score_d<true>(P, stream);
+  if (e != hipSuccess) return e;
+  return launch_select<true>(P, stream);
 }
 
 }  // namespace ugbs

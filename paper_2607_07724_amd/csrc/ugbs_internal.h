@@ -27,7 +27,11 @@ hipError_t launch_block_meta(const Shape& s, const uint16_t* K, uint16_t* meta,
                              hipStream_t stream);
 hipError_t launch_score_select(const Shape& s, const uint16_t* Q, const uint16_t* meta,
                                const float* scores_in, float* scores_out,
-                               int32_t* idx_sorted, float* sigma, hipStream_t stream);
+                               int32_t* idx_sorted, float* sigma, void* workspace,
+                               hipStream_t stream);
+// Bytes of packed candidate scores the score kernel writes into the workspace
+// when the caller supplies neither scores_in nor scores_out.
+size_t score_scratch_bytes(const Shape& s);
 hipError_t launch_route(const Shape& s, int n_pop, int n_trig, const float* sigma,
                         const int32_t* idx_sorted, int32_t* kv_idx, float* sigma_bar,
                         float* tau, uint8_t* trigger, void* workspace, hipStream_t stream);
@@ -42,7 +46,13 @@ inline size_t ws_tau_off(const Shape& s) { return ws_align(sizeof(float) * size_
 inline size_t ws_trigger_off(const Shape& s) {
   return ws_tau_off(s) + ws_align(sizeof(float) * size_t(s.B));
 }
-inline size_t ws_total(const Shape& s) { return ws_trigger_off(s) + ws_align(size_t(s.B) * s.T); }
+inline size_t ws_route_total(const Shape& s) { return ws_trigger_off(s) + ws_align(size_t(s.B) * s.T); }
+// One workspace serves both calls: the packed scores are dead once
+// ugbs_score_select returns, and ugbs_route only needs its own sections.
+inline size_t ws_total(const Shape& s) {
+  const size_t a = ws_route_total(s), b = ws_align(score_scratch_bytes(s));
+  return a > b ? a : b;
+}
 
 // Work-unit ordering used by the per-(tile, head) kernels: consecutive
 // workgroup ids are dealt round-robin to the 8 XCDs, so the id is remapped

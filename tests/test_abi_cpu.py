@@ -87,7 +87,7 @@ def test_invalid_problem_rejected_by_every_entry_point(kw, code):
     fake = ctypes.c_void_p(0x100000)        # never dereferenced: validation fails first
     want = _enum(code)
     assert L.ugbs_block_meta(ctypes.byref(p), fake, fake, None) == want
-    assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, fake, fake, None) == want
+    assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, fake, fake, fake, 1 << 30, None) == want
     assert L.ugbs_route(ctypes.byref(p), fake, fake, fake, None, None, None, fake, 1 << 20, None) == want
     assert L.ugbs_attend(ctypes.byref(p), fake, fake, fake, fake, 8, fake, None) == want
     assert L.ugbs_workspace_bytes(ctypes.byref(p)) == 0
@@ -101,9 +101,9 @@ def test_null_problem_and_null_pointers():
     p = good()
     assert L.ugbs_block_meta(ctypes.byref(p), None, fake, None) == ERR_NULL
     assert L.ugbs_block_meta(ctypes.byref(p), fake, None, None) == ERR_NULL
-    assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, None, fake, None) == ERR_NULL
-    assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, fake, None, None) == ERR_NULL
-    assert L.ugbs_score_select(ctypes.byref(p), None, fake, None, None, fake, fake, None) == ERR_NULL
+    assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, None, fake, fake, 1 << 30, None) == ERR_NULL
+    assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, fake, None, fake, 1 << 30, None) == ERR_NULL
+    assert L.ugbs_score_select(ctypes.byref(p), None, fake, None, None, fake, fake, fake, 1 << 30, None) == ERR_NULL
     assert L.ugbs_route(ctypes.byref(p), None, fake, fake, None, None, None, fake, 1 << 20, None) == ERR_NULL
     assert L.ugbs_route(ctypes.byref(p), fake, fake, None, None, None, None, fake, 1 << 20, None) == ERR_NULL
     for i in range(5):
@@ -125,7 +125,12 @@ def test_workspace_and_alignment_and_width_checks():
     assert L.ugbs_route(ctypes.byref(p), fake, fake, fake, None, None, None, ctypes.c_void_p(0x100010),
                         need, None) == ERR_ALIGN
     assert L.ugbs_block_meta(ctypes.byref(p), ctypes.c_void_p(0x100008), fake, None) == ERR_ALIGN
-    assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, odd, fake, None) == ERR_ALIGN
+    assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, odd, fake, fake, need, None) == ERR_ALIGN
+    # without scores_in / scores_out the scores pass through the workspace
+    assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, fake, fake, None, 0, None) == ERR_WS
+    assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, fake, fake, fake, need - 1, None) == ERR_WS
+    assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, fake, fake,
+                               ctypes.c_void_p(0x100010), need, None) == ERR_ALIGN
     assert L.ugbs_attend(ctypes.byref(p), fake, fake, fake, odd, 8, fake, None) == ERR_ALIGN
     assert L.ugbs_attend(ctypes.byref(p), fake, fake, fake, fake, 0, fake, None) == ERR_SHAPE
     assert L.ugbs_attend(ctypes.byref(p), fake, fake, fake, fake, 4097, fake, None) == ERR_SHAPE
@@ -136,6 +141,19 @@ def test_workspace_bytes_grows_with_tiles():
     b = ugbs.ugbs_workspace_bytes(ugbs.Problem.make(2, 4, 1, 131072, 64, 4, 0.25))
     assert 0 < a < b
     assert b >= 2 * 2048 * 4 + 2 * 2048
+
+
+@pytest.mark.parametrize("B,H,N", [(1, 4, 1024), (2, 32, 131072), (1, 28, 65536), (1, 2, 64), (1, 2, 128)])
+def test_workspace_holds_the_packed_candidate_scores(B, H, N):
+    """B H (T-1)(T-2)/2 fp32 candidate scores (rows t = 2..T-1 hold t-1 each),
+    and the route sections, whichever is larger, rounded up to 256 bytes."""
+    T = N // 64
+    packed = 4 * B * H * sum(max(t - 1, 0) for t in range(T))
+    route = 4 * B * T + 4 * B + B * T
+    got = ugbs.ugbs_workspace_bytes(ugbs.Problem.make(B, H, 1, N, 64, 3, 0.25))
+    assert got % 256 == 0
+    assert got >= max(packed, route)
+    assert got < max(packed, route) + 3 * 256
 
 
 def test_binding_rejects_host_tensors_before_calling():

@@ -103,7 +103,10 @@ def _select_gpu(w, p, Q, meta_np, scores_in=None, want_scores=False):
     sig = torch.empty((w.B, w.H, w.T), dtype=torch.float32, device="cuda")
     so = torch.empty((w.B, w.H, w.T, w.NB), dtype=torch.float32, device="cuda") if want_scores else None
     si = dev(scores_in) if scores_in is not None else None
-    ugbs.ugbs_score_select(p, Q, meta, idx, sig, scores_in=si, scores_out=so)
+    ws = None
+    if si is None and so is None:
+        ws = torch.empty((ugbs.ugbs_workspace_bytes(p),), dtype=torch.uint8, device="cuda")
+    ugbs.ugbs_score_select(p, Q, meta, idx, sig, scores_in=si, scores_out=so, workspace=ws)
     torch.cuda.synchronize()
     return host(idx), host(sig), (host(so) if want_scores else None)
 
@@ -166,6 +169,24 @@ def test_tile_scores_within_fp32_accumulation_bound(name, backbone):
             err = np.abs(so[b, h].astype(np.float64) - S[b, h].astype(np.float64))
             err[~fin[b, h]] = 0
             assert np.all(err <= bound), (b, h, float((err / bound).max()))
+
+
+@pytest.mark.parametrize("name", list(CASES))
+@pytest.mark.parametrize("backbone", [synth.KMEAN, synth.QUEST])
+def test_workspace_scores_path_matches_scores_out_path(name, backbone):
+    """Scores routed through the packed workspace rows and through the
+    caller's [.., N_B] tensor feed the same selection: identical idx_sorted
+    and sigma (the selection itself is checked against the oracle through
+    scores_in above)."""
+    c = case(name)
+    w = c["w"].replace(backbone=backbone)
+    p = problem(w)
+    meta = oracle.block_meta(backbone, c["inp"].K)
+    Q = dev_bf16(c["inp"].Q)
+    i1, s1, _ = _select_gpu(w, p, Q, meta, want_scores=True)
+    i2, s2, _ = _select_gpu(w, p, Q, meta)
+    assert np.array_equal(i1, i2)
+    assert np.array_equal(s1.view(np.uint32), s2.view(np.uint32))
 
 
 # ---------------------------------------------------------------- stage 4
