@@ -28,9 +28,8 @@
 // |F|, |C|)), the R-th largest key is found among the survivors by a
 // most-significant-bit-first radix descent that counts with wave ballots,
 // the top R are compacted (equal keys at the threshold by lower block
-// index) and ordered by (key, ~index): for R <= 128 each survivor's rank is
-// counted in registers from readlane broadcasts and it is scattered into
-// place, otherwise a bitonic sort in LDS.  sigma uses IEEE fp32 subtract and
+// index) and ordered by (key, ~index) with a bitonic sort: in registers
+// across lanes for R <= 128, in LDS above.  sigma uses IEEE fp32 subtract and
 // divide.  Splitting the stages keeps each kernel at its own occupancy (the
 // scoring kernel is bound by registers, the selection kernel by latency).
 #include "ugbs_internal.h"
@@ -118,17 +117,13 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
   return x;
 }
 
-// R largest of the keys held in key[0..nslots) (0 = empty; entries in
-// position order slot by slot, lane by lane), written to s_sel[0..R) as
-// (key << 32) | ~position, unsorted: a most-significant-bit-first radix
-// descent finds the R-th largest key thr by counting with wave ballots,
-// then keys above thr and the lowest-position keys equal to thr are
-// compacted.
+// Largest thr with at least R of the keys held in key[0..nslots) at or above
+// it (0 = empty slot): a most-significant-bit-first radix descent that
+// counts with wave ballots.  *exact: exactly R keys are >= thr.
 template <int S>
-__device__ __forceinline__ void select_top(const uint32_t (&key)[S], const uint32_t (&pos)[S],
-                                           int nslots, int R, uint64_t* s_sel, int lane) {
+__device__ __forceinline__ uint32_t kth_largest(const uint32_t (&key)[S], int nslots, int R, bool* exact) {
   uint32_t thr = 0;
-  bool exact = false;
+  *exact = false;
   for (int bit = 31; bit >= 0; --bit) {
     const uint32_t cand = thr | (1u << bit);
     int cnt = 0;
@@ -138,11 +133,24 @@ __device__ __forceinline__ void select_top(const uint32_t (&key)[S], const uint3
     if (cnt >= R) {
       thr = cand;
       if (cnt == R) {
-        exact = true;
+        *exact = true;
         break;
       }
     }
   }
+  return thr;
+}
+
+// R largest of the keys held in key[0..nslots) (0 = empty; entries in
+// position order slot by slot, lane by lane), written to s_sel[0..R) as
+// (key << 32) | ~position, unsorted: the R-th largest key thr comes from
+// kth_largest, then keys above thr and the lowest-position keys equal to
+// thr are compacted.
+template <int S>
+__device__ __forceinline__ void select_top(const uint32_t (&key)[S], const uint32_t (&pos)[S],
+                                           int nslots, int R, uint64_t* s_sel, int lane) {
+  bool exact;
+  const uint32_t thr = kth_largest<S>(key, nslots, R, &exact);
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   int base = 0;
 #pragma unroll
@@ -399,34 +407,44 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
   }
 
   // ---- the R largest keys, compacted into s_sel as (key, ~position) -------
-  // Pre-filter: with P = ceil(R / 64) <= 2, the smallest over lanes of each
-  // lane's P-th largest key, T0, has at least 64 P >= R keys at or above it,
-  // so the R largest are among {key >= T0} (typically a few hundred of up to
-  // 2046).  Those survivors, in position order, go through the exact
-  // selection; otherwise every candidate does.
+  // Pre-filter: each lane's three largest keys form a subset of the keys, so
+  // the R-th largest of those 192 values, T0, is at most the R-th largest
+  // key (R <= 192): the R largest are among {key >= T0}, typically R plus a
+  // few dozen of up to 2046.  Those survivors, in position order, go
+  // through the exact selection; otherwise every candidate does.
   constexpr int kMaxSlots = UGBS_MAX_BLOCKS / 64;
   const int nslots = (nc + 63) / 64;
   uint32_t keys[kMaxSlots];
+  {
+    // every load first (clamped in-row addresses), then the conversions, so
+    // the loads are in flight together
+    float raw[kMaxSlots];
 #pragma unroll
-  for (int sl = 0; sl < kMaxSlots; ++sl) {
-    const int p = 64 * sl + lane;
-    keys[sl] = (sl < nslots && p < nc) ? order_key(src[p]) : 0u;  // valid keys are >= 0x007fffff
+    for (int sl = 0; sl < kMaxSlots; ++sl) {
+      const int p = 64 * sl + lane;
+      raw[sl] = (sl < nslots) ? src[p < nc ? p : nc - 1] : 0.f;
+    }
+#pragma unroll
+    for (int sl = 0; sl < kMaxSlots; ++sl) {
+      const int p = 64 * sl + lane;
+      keys[sl] = (sl < nslots && p < nc) ? order_key(raw[sl]) : 0u;  // valid keys are >= 0x007fffff
+    }
   }
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   bool filtered = false;
-  if (R <= 128 && nc > R) {
-    uint32_t m1 = 0, m2 = 0;
+  if (R <= 192 && nc > R) {
+    uint32_t top3[3] = {0u, 0u, 0u};
 #pragma unroll
     for (int sl = 0; sl < kMaxSlots; ++sl) {
       if (sl < nslots) {
         const uint32_t x = keys[sl];
-        const uint32_t lo = min(m1, x);
-        m1 = max(m1, x);
-        m2 = max(m2, lo);
+        top3[2] = max(top3[2], min(top3[1], x));
+        top3[1] = max(top3[1], min(top3[0], x));
+        top3[0] = max(top3[0], x);
       }
     }
-    uint32_t t0 = (R <= 64) ? m1 : m2;
-    t0 = wave_min_u32(t0);
+    bool exact0;
+    const uint32_t t0 = kth_largest<3>(top3, 3, R, &exact0);
     if (t0 > 0u) {
       int ns = 0;
 #pragma unroll
@@ -463,23 +481,43 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
     select_top<kMaxSlots>(keys, pos, nslots, R, s_sel, lane);
   }
   if (R <= 128) {
-    // ---- rank each of the R survivors (2 per lane) by counting larger
-    // (key, ~index) pairs broadcast with readlane, then scatter into order
+    // ---- bitonic sort of the R winners (2 per lane, slot-major index
+    // i = 64 slot + lane; empty entries are 0 and sort last), descending;
+    // partners within a slot are exchanged across lanes, across slots in
+    // registers
     wave_lds_sync();
-    const uint64_t e0 = (lane < R) ? s_sel[lane] : 0ull;
-    const uint64_t e1 = (64 + lane < R) ? s_sel[64 + lane] : 0ull;
-    int r0 = 0, r1 = 0;
-    for (int j = 0; j < R; ++j) {
-      const uint64_t src = (j < 64) ? e0 : e1;     // j is wave-uniform
-      const int jl = j & 63;
-      const uint64_t x = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(src >> 32), jl) << 32) |
-                         (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)src, jl);
-      r0 += (x > e0) ? 1 : 0;
-      r1 += (x > e1) ? 1 : 0;
+    uint64_t e[2];
+    e[0] = (lane < R) ? s_sel[lane] : 0ull;
+    e[1] = (64 + lane < R) ? s_sel[64 + lane] : 0ull;
+#pragma unroll
+    for (int size = 2; size <= 128; size <<= 1) {
+#pragma unroll
+      for (int stride = size >> 1; stride > 0; stride >>= 1) {
+        if (stride == 64) {
+          // i = lane, j = 64 + lane, (i & 128) == 0: descending
+          const uint64_t hi = e[0] > e[1] ? e[0] : e[1];
+          const uint64_t lo = e[0] > e[1] ? e[1] : e[0];
+          e[0] = hi;
+          e[1] = lo;
+        } else {
+          const bool lower = (lane & stride) == 0;
+#pragma unroll
+          for (int sl = 0; sl < 2; ++sl) {
+            const int i = 64 * sl + lane;
+            const bool desc = (i & size) == 0;
+            const uint32_t plo = (uint32_t)__shfl_xor((int)(uint32_t)e[sl], stride);
+            const uint32_t phi = (uint32_t)__shfl_xor((int)(uint32_t)(e[sl] >> 32), stride);
+            const uint64_t pv = ((uint64_t)phi << 32) | plo;
+            const bool keep_max = (lower == desc);
+            const bool take = keep_max ? (pv > e[sl]) : (pv < e[sl]);
+            e[sl] = take ? pv : e[sl];
+          }
+        }
+      }
     }
     wave_lds_sync();
-    if (lane < R) s_sel[r0] = e0;
-    if (64 + lane < R) s_sel[r1] = e1;
+    s_sel[lane] = e[0];
+    s_sel[64 + lane] = e[1];
     wave_lds_sync();
   } else {
     int n2 = 2;
