@@ -18,7 +18,7 @@
 // the 16-byte column c of row r sits at c ^ (r mod 16), which makes the
 // operand reads bank-conflict free.  The max over the tile's rows (A.3) is
 // the max over a lane's 16 accumulators and then across the four 16-lane
-// groups; the 16 tile scores of a chunk go to memory as one 64-byte store,
+// groups; the row of tile scores collects in LDS and goes to memory once,
 // into the caller's [.., N_B] score tensor or into packed rows of the
 // workspace (row (b, h, t) holds the t-1 candidates 1..t-1).
 //
@@ -58,6 +58,7 @@ struct SelParams {
   int n_wg;       // score-kernel workgroups
   int wave_lds;   // bytes of per-wave LDS of the selection kernel (survivors)
   int ring_lds;   // bytes of the metadata ring
+  int row_lds;    // bytes of per-wave LDS of the score kernel (one row of scores)
 };
 
 // Offset (floats) of the packed candidate row of unit (bh, t): rows of one
@@ -276,6 +277,10 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
   const int nc = (t >= 1) ? t - 1 : 0;
 
   unsigned char* ring = smem;
+  // this wave's tile scores stay in LDS until the chunk loop is done, so the
+  // only vector-memory operations in flight there are the ring's loads (the
+  // loop's vmcnt waits count nothing else)
+  float* s_row = reinterpret_cast<float*>(smem + P.ring_lds + w * P.row_lds);
 
   // this unit's candidate scores 1..nc: packed rows, or the full [.., N_B] row
   float* dst = PACKED ? P.scratch + packed_row(gr.b * s.H + h, t, s.T) : P.scores_out + row * s.NB + 1;
@@ -361,8 +366,13 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
           for (int i = 0; i < 4; ++i) mx = fmaxf(mx, acc[rt][i]);
         mx = wave_max16(mx);
         const int pos = kChunk * c + c16;
-        if (g == 0 && pos < nc) dst[pos] = mx;
+        if (g == 0 && pos < nc) s_row[pos] = mx;
       }
+    }
+    if (active) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      __builtin_amdgcn_wave_barrier();
+      for (int p = lane; p < nc; p += 64) dst[p] = s_row[p];
     }
   }
   if (!active || PACKED) return;
@@ -572,7 +582,13 @@ template <int D, bool QUEST, bool PACKED>
 hipError_t launch_score(SelParams P, hipStream_t stream) {
   using MC = MetaChunk<D, QUEST>;
   P.ring_lds = kRing * MC::kBytes;
-  const size_t smem = (size_t)P.ring_lds;
+  P.row_lds = (P.s.NB * 4 + 15) & ~15;
+  const size_t smem = (size_t)P.ring_lds + (size_t)P.GW * P.row_lds;
+  if (smem > 65536) {
+    const hipError_t e = hipFuncSetAttribute((const void*)score_kernel<D, QUEST, PACKED>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+  }
   const int grid = ((P.n_wg + 7) / 8) * 8;
   score_kernel<D, QUEST, PACKED><<<grid, 64 * P.GW, smem, stream>>>(P);
   return hipGetLastError();
@@ -633,6 +649,7 @@ hipError_t launch_score_select(const Shape& s, const uint16_t* Q, const uint16_t
   if (sel_bytes < 8 * kSurvivors) sel_bytes = 8 * kSurvivors;
   P.wave_lds = sel_bytes;
   P.ring_lds = 0;
+  P.row_lds = 0;
   if (scores_in) return launch_select<false>(P, stream);
   if (scores_out) {
     const hipError_t e = launch_score_d<false>(P, stream);
