@@ -34,6 +34,8 @@ def lib():
         L.orc_select.argtypes = [i32, i32, i64, P, P, P, P]
         L.orc_route.argtypes = [i32, i32, i32, i32, f64, P, P, P, P, P, P]
         L.orc_attend.argtypes = [i32, i32, i32, i32, f64, P, P, P, P, i32, i32, i64, P, P, i32]
+        L.orc_row_roughness.argtypes = [i32, i32, i32, i32, i32, P, P, i64, P, P, i32]
+        L.orc_row_roughness.restype = ctypes.c_int
         L.orc_bf16_round.argtypes = [f64]
         L.orc_bf16_round.restype = ctypes.c_uint16
         for f in ("orc_block_meta", "orc_tile_scores", "orc_select", "orc_route", "orc_attend"):
@@ -162,6 +164,25 @@ def attend(Q, K, V, kv_idx=None, scale=None, units=None, dense=False, nthreads=N
     if full:
         return O.reshape(B, H, NB * BLOCK, d)
     return O
+
+
+def row_roughness(backbone, Q, meta, Hkv, units=None, nthreads=None):
+    """Appendix D step 3: per unit (b, h, t), sum over candidate blocks of
+    C(t) and the 63 adjacent row pairs of the tile of (s[r+1,b] - s[r,b])^2
+    (per-row block scores, fp64).  Returns (sums [n_units] f64, terms [n_units])."""
+    Q = _c(Q, np.uint16)
+    meta = _c(meta, np.uint16)
+    B, H, N, d = Q.shape
+    T = N // BLOCK
+    if units is None:
+        units = all_units(B, H, T)
+    units = _c(np.asarray(units, np.int32), np.int32)
+    out = np.empty(units.shape[0], np.float64)
+    rc = lib().orc_row_roughness(backbone, H, Hkv, N, d, _ptr(Q), _ptr(meta), units.shape[0],
+                                 _ptr(units), _ptr(out), nthreads or default_threads())
+    assert rc == 0
+    terms = 63 * np.maximum(units[:, 2].astype(np.int64) - 1, 0)
+    return out, terms
 
 
 def population(T, k):

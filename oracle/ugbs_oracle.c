@@ -23,6 +23,8 @@
  *   A.7, A.8       head mean and per-layer empirical quantile, Eq. (trigger)
  *   A.9            padded expansion with sentinel N_B
  *   A.10           exact softmax attention over the kept blocks, Eq. (Attn)
+ *   App. D         per-row score roughness for the noise-scale estimate
+ *                  (empirical recipe, step 3)
  *
  * Readings where the paper is silent (each one also stated in the design
  * notes of the repository):
@@ -432,4 +434,62 @@ int orc_attend(int H, int Hkv, int N, int d, double scale, const uint16_t* Q,
 }
 
 /* Exposed for the oracle's own pins: bf16 rounding of a double. */
+/* ------------------------------------------------------------------ */
+/* Appendix D, empirical recipe step 3: row-to-row score roughness     */
+/* ------------------------------------------------------------------ */
+/* For each requested unit (b, h, t): the sum over candidate blocks b' in
+ * C(t) = {1..t-1} and over the 63 adjacent row pairs (r, r+1) of tile t of
+ * (s[r+1, b'] - s[r, b'])^2, with the per-row block score s of A.2 (the same
+ * formula as the tile score, before the max over rows), all in double.  The
+ * number of terms is 63 |C(t)|. */
+typedef struct {
+  int backbone, H, Hkv, N, d;
+  const uint16_t* Q;
+  const uint16_t* meta;
+  const int32_t* units;
+  double* out;
+} rough_ctx;
+
+static void rough_item(long u, void* vctx) {
+  rough_ctx* c = (rough_ctx*)vctx;
+  int NB = c->N / ORC_BLOCK, d = c->d, G = c->H / c->Hkv;
+  int b = c->units[3 * u], h = c->units[3 * u + 1], t = c->units[3 * u + 2];
+  int kvh = h / G;
+  double* q = (double*)malloc(sizeof(double) * (size_t)ORC_BLOCK * d);
+  const uint16_t* qb = c->Q + (((size_t)b * c->H + h) * c->N + (size_t)t * ORC_BLOCK) * d;
+  for (long x = 0; x < (long)ORC_BLOCK * d; ++x) q[x] = bf16_val(qb[x]);
+  int width = (c->backbone == ORC_KMEAN) ? 1 : 2;
+  double total = 0.0;
+  for (int blk = 1; blk <= t - 1; ++blk) {
+    const uint16_t* m = c->meta + (((size_t)b * c->Hkv + kvh) * NB + blk) * width * d;
+    double prev = 0.0;
+    for (int r = 0; r < ORC_BLOCK; ++r) {
+      const double* qr = q + (size_t)r * d;
+      double s = 0.0;
+      if (c->backbone == ORC_KMEAN) {
+        for (int e = 0; e < d; ++e) s += qr[e] * bf16_val(m[e]);
+      } else {
+        for (int e = 0; e < d; ++e) {
+          double a = qr[e] * bf16_val(m[d + e]);
+          double z = qr[e] * bf16_val(m[e]);
+          s += (a > z) ? a : z;
+        }
+      }
+      if (r > 0) total += (s - prev) * (s - prev);
+      prev = s;
+    }
+  }
+  c->out[u] = total;
+  free(q);
+}
+
+int orc_row_roughness(int backbone, int H, int Hkv, int N, int d, const uint16_t* Q,
+                      const uint16_t* meta, long n_units, const int32_t* units, double* out,
+                      int nthreads) {
+  if (N % ORC_BLOCK || H % Hkv) return -1;
+  rough_ctx c = {backbone, H, Hkv, N, d, Q, meta, units, out};
+  orc_parallel(n_units, nthreads, rough_item, &c);
+  return 0;
+}
+
 uint16_t orc_bf16_round(double x) { return bf16_round(x); }
