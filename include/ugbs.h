@@ -18,6 +18,12 @@
  *   ugbs_attend       (Q, K, V, kv_idx)      -> O
  * No call synchronises the device; none allocates device memory.
  *
+ * Diagnostics (Appendix D: sigma as a best-arm identification index), off
+ * the prefill path, on the score tensor of ugbs_score_select(scores_out):
+ *   ugbs_noise_scale  (Q, meta)                 -> rough, tau
+ *   ugbs_bai_tiles    (scores, tau, z)          -> per-tile gaps, MC failures
+ *   ugbs_bai_heads    (tiles, tau)              -> per-head aggregates
+ *
  * Conventions shared by every entry point
  *   - All tensor pointers are device pointers owned by the caller.  The
  *     library never frees, keeps or allocates them.
@@ -51,7 +57,7 @@ extern "C" {
 #define UGBS_API
 #endif
 
-#define UGBS_ABI_VERSION 2
+#define UGBS_ABI_VERSION 3
 #define UGBS_BLOCK 64          /* BLOCK_M = BLOCK_N = 64 tokens (Section 3.1, 3.2) */
 #define UGBS_MAX_BLOCKS 2048   /* N_B <= 2048, i.e. N <= 131072 */
 #define UGBS_MAX_KV_WIDTH 4096 /* kv_width accepted by ugbs_attend; k_budget <= 2048 */
@@ -177,6 +183,96 @@ UGBS_API int ugbs_route(const ugbs_problem* p, const float* sigma, const int32_t
  *   O       : [B, H, N, d] bf16, 16-byte aligned; fully written. */
 UGBS_API int ugbs_attend(const ugbs_problem* p, const void* Q, const void* K, const void* V,
                 const int32_t* kv_idx, int32_t kv_width, void* O, void* stream);
+
+/* ---- Diagnostics (Appendix D) ----------------------------------------------
+ * With F(t) the forced list, m = k - |F| kept candidates and
+ * R' = rho k - |F| candidates after expansion (rho = 2), a tile enters the
+ * diagnostics when |C(t)| >= R' + 1 (at least rho k + 1 visible blocks, the
+ * paper's diagnostic mask).  For such a tile, with c the candidate scores
+ * sorted as in ugbs_score_select (descending, lower block first on ties):
+ *   g = c[m-1] - c[m], G = c[m-1] - c[R'], r = c[0] - c[m]   (Eq. (gaps))
+ *   sigma = g / r (0 when r == 0), all fp32 subtract / IEEE divide. */
+typedef struct ugbs_bai_tile {
+  float g, G, r, sigma;
+  float delta2;     /* min over j = 0..R'-1, j != m-1, of c[j] - c[j+1]: the
+                       smallest secondary spacing, assumption (A1) */
+  int32_t fail_k;   /* Monte Carlo samples in which the empirical top-m set
+                       misses the true top-m of mu (see ugbs_bai_tiles) */
+  int32_t fail_rk;  /* samples in which the empirical top-R' set misses it */
+  int32_t valid;    /* 1 if the tile is in the diagnostic mask; otherwise 0,
+                       the floats NaN and the counts 0 */
+} ugbs_bai_tile;
+
+/* Per (batch, head) aggregates over the n_tiles valid tiles of a sequence
+ * (the empirical recipe of Appendix D).  Fields that are undefined for a
+ * head (no valid tile; n_q = 0; tau not positive; n_samples = 0) are NaN. */
+typedef struct ugbs_bai_head {
+  int32_t n_tiles;     /* valid tiles n */
+  int32_t n_q;         /* ceil(q n), the router's trigger count */
+  int32_t pad[2];
+  double r_mean;       /* mean of r (left-to-right fp64 sum in tile order) / n */
+  double r_cv;         /* sqrt(mean (r - r_mean)^2) / r_mean: the proxy for beta in (A2) */
+  double sigma_q;      /* the n_q-th smallest sigma (lower tile first on ties) */
+  double gamma_q;      /* sigma_q * r_mean */
+  double band_mass;    /* fraction of tiles with g in [gamma_q (1-beta), gamma_q (1+beta)] */
+  double delta2_p05;   /* delta2 at sorted position floor(0.05 (n-1)): the Delta_2 used */
+  double delta2_p50;   /* delta2 at sorted position floor(0.5 (n-1)) */
+  double pi2;          /* fraction of tiles with delta2 < delta2_p05 (the pi_2 term) */
+  double tau;          /* the noise scale used, as given */
+  double chi;          /* sum_{j>=1} (j+1) exp(-j^2 Delta_2^2 / (4 tau^2)); +inf when
+                          Delta_2 <= 0 or more than 1e6 terms are needed */
+  double eps_bar;      /* chi + (1 + chi) exp(-((rho-1) k Delta_2)^2 / (4 tau^2)) */
+  double vbar_gamma;   /* Vbar(gamma_q) = Phi(-gamma_q / (sqrt2 tau)) */
+  double C_q;          /* min{1, (1+eps_bar)/2, sqrt2 beta gamma_q / tau
+                          phi(gamma_q (1-beta) / (sqrt2 tau)) + eps_bar} */
+  double bound;        /* min(q, 1-q) C_q + pi2 (the Proposition, with pi_2) */
+  double bound_band;   /* band_mass / 2 C_q + pi2 */
+  double mc_err_k;     /* sum fail_k / (n n_samples) */
+  double mc_err_rk;    /* sum fail_rk / (n n_samples) */
+  double mc_regret;    /* R_q: with V = (fail_k - fail_rk) / n_samples per tile,
+                          (sum of the n_q largest V - sum of V over the router's
+                          n_q tiles) / n */
+} ugbs_bai_head;
+
+/* Noise scale tau from row-to-row score differences (Appendix D, empirical
+ * recipe step 3): adjacent query rows of a tile see the same block, so the
+ * difference of their scores carries two independent noise draws and
+ * E[(s[r+1,b] - s[r,b])^2] = 2 tau^2.
+ *   rough : [B, H, T] fp64, 8-byte aligned, fully written.  For tile t:
+ *           the sum over candidate blocks b in C(t) = {1..t-1} and the 63
+ *           adjacent row pairs (r, r+1) of (s[r+1,b] - s[r,b])^2, where s is
+ *           the per-row block score of ugbs_score_select (before the max over
+ *           rows), fp32 scores and squares, fp64 accumulation; 0 for t < 2.
+ *   tau   : [B, H] fp32, fully written: sqrt(sum_t rough / (2 * 63 *
+ *           (T-1)(T-2)/2)), NaN when T < 3.
+ *   Q, meta as for ugbs_score_select. */
+UGBS_API int ugbs_noise_scale(const ugbs_problem* p, const void* Q, const void* meta,
+                              double* rough, float* tau, void* stream);
+
+/* Per-tile gaps and Monte Carlo identification failures.
+ *   scores    : [B, H, T, N_B] fp32 tile scores in the layout of
+ *               ugbs_score_select's scores_out (entries of C(t) are read).
+ *   tau       : [B, H] fp32 noise scale; may be NULL when n_samples == 0.
+ *   z         : [n_samples, N_B] fp32 standard normals shared by all tiles
+ *               and heads; may be NULL when n_samples == 0.
+ *   n_samples : 0 <= n_samples <= 1 << 20.
+ *   tiles     : [B, H, T] ugbs_bai_tile, 8-byte aligned, fully written.
+ * For sample s the perturbed scores are mu_b = fp32(c_b + fp32(tau z[s, b]))
+ * over b in C(t) (c_b with -0 read as +0).  fail_k counts the samples where
+ * NOT (min of mu over the empirical top-m > max of mu over the other
+ * candidates); fail_rk the samples where fewer than m members of the
+ * empirical top-R' exceed every other candidate's mu. */
+UGBS_API int ugbs_bai_tiles(const ugbs_problem* p, const float* scores, const float* tau,
+                            const float* z, int32_t n_samples, ugbs_bai_tile* tiles, void* stream);
+
+/* Per-head aggregates (ugbs_bai_head) from the tiles of ugbs_bai_tiles; q and
+ * k_budget come from p.
+ *   tiles     : [B, H, T] from ugbs_bai_tiles for the same problem.
+ *   tau       : [B, H] fp32, the noise scale for the closed forms.
+ *   n_samples : the value passed to ugbs_bai_tiles.
+ *   heads     : [B, H] ugbs_bai_head, 8-byte aligned, fully written. */
+UGBS_API int ugbs_bai_heads(const ugbs_problem* p, const ugbs_bai_tile* tiles, const float* tau,
+                            int32_t n_samples, ugbs_bai_head* heads, void* stream);
 
 /* Bytes of device workspace ugbs_score_select (without scores_in/scores_out)
  * and ugbs_route need for problem p; one workspace serves both calls in

@@ -20,6 +20,8 @@ __all__ = [
     "KMEAN", "QUEST", "BLOCK", "Problem", "UGBSError", "lib", "library_path",
     "ugbs_block_meta", "ugbs_score_select", "ugbs_route", "ugbs_attend",
     "ugbs_workspace_bytes", "ugbs_status_string", "ugbs_abi_version",
+    "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads", "BAI_TILE_FIELDS", "BAI_HEAD_FIELDS",
+    "bai_tile_records", "bai_head_records",
 ]
 
 KMEAN, QUEST = 0, 1
@@ -104,7 +106,11 @@ def lib():
         L.ugbs_status_string.argtypes = [ctypes.c_int]
         L.ugbs_status_string.restype = ctypes.c_char_p
         L.ugbs_abi_version.argtypes = []
-        for f in ("ugbs_block_meta", "ugbs_score_select", "ugbs_route", "ugbs_attend", "ugbs_abi_version"):
+        L.ugbs_noise_scale.argtypes = [pp, P, P, P, P, P]
+        L.ugbs_bai_tiles.argtypes = [pp, P, P, P, ctypes.c_int32, P, P]
+        L.ugbs_bai_heads.argtypes = [pp, P, P, ctypes.c_int32, P, P]
+        for f in ("ugbs_block_meta", "ugbs_score_select", "ugbs_route", "ugbs_attend", "ugbs_abi_version",
+                  "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -227,6 +233,81 @@ def ugbs_attend(p: Problem, Q, K, V, kv_idx, O, stream=None):
     kv = _check("kv_idx", kv_idx, (p.batch, p.n_heads, p.T, width), (torch.int32,), dev)
     o = _check("O", O, (p.batch, p.n_heads, p.seq_len, p.head_dim), bf, dev)
     _raise("ugbs_attend", lib().ugbs_attend(ctypes.byref(p), q, k, v, kv, width, o, _stream(stream)))
+
+
+# ---------------------------------------------------------------- diagnostics
+
+# Field layout of ugbs_bai_tile (32 bytes) and ugbs_bai_head (160 bytes).
+BAI_TILE_FIELDS = [("g", "<f4"), ("G", "<f4"), ("r", "<f4"), ("sigma", "<f4"), ("delta2", "<f4"),
+                   ("fail_k", "<i4"), ("fail_rk", "<i4"), ("valid", "<i4")]
+BAI_HEAD_FIELDS = [("n_tiles", "<i4"), ("n_q", "<i4"), ("pad", "<i4", (2,))] + [
+    (n, "<f8") for n in ("r_mean", "r_cv", "sigma_q", "gamma_q", "band_mass", "delta2_p05",
+                         "delta2_p50", "pi2", "tau", "chi", "eps_bar", "vbar_gamma", "C_q", "bound",
+                         "bound_band", "mc_err_k", "mc_err_rk", "mc_regret")]
+BAI_TILE_BYTES, BAI_HEAD_BYTES = 32, 160
+
+
+def _bytes_buf(name, t, n_bytes, dev):
+    if t is None or not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous device tensor")
+    if t.numel() * t.element_size() != n_bytes:
+        raise ValueError(f"{name} must hold exactly {n_bytes} bytes")
+    if t.device != dev:
+        raise ValueError(f"{name} is on {t.device}, expected {dev}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def bai_tile_records(tiles):
+    """Host copy of a ugbs_bai_tile buffer as a numpy structured array [..]."""
+    import numpy as np
+    raw = tiles.detach().cpu().contiguous().view(-1).numpy().view(np.uint8)
+    return raw.view(np.dtype(BAI_TILE_FIELDS))
+
+
+def bai_head_records(heads):
+    """Host copy of a ugbs_bai_head buffer as a numpy structured array [..]."""
+    import numpy as np
+    raw = heads.detach().cpu().contiguous().view(-1).numpy().view(np.uint8)
+    return raw.view(np.dtype(BAI_HEAD_FIELDS))
+
+
+def ugbs_noise_scale(p: Problem, Q, meta, rough, tau, stream=None):
+    """Appendix D step 3: rough [B,H,T] fp64 (per-tile sums of squared
+    row-to-row score differences), tau [B,H] fp32."""
+    import torch
+    bf = _bf16()
+    dev = Q.device
+    q = _check("Q", Q, (p.batch, p.n_heads, p.seq_len, p.head_dim), bf)
+    m = _check("meta", meta, (p.batch, p.n_kv_heads, p.NB, p.meta_width, p.head_dim), bf, dev)
+    r = _check("rough", rough, (p.batch, p.n_heads, p.T), (torch.float64,), dev)
+    ta = _check("tau", tau, (p.batch, p.n_heads), (torch.float32,), dev)
+    _raise("ugbs_noise_scale", lib().ugbs_noise_scale(ctypes.byref(p), q, m, r, ta, _stream(stream)))
+
+
+def ugbs_bai_tiles(p: Problem, scores, tiles, tau=None, z=None, stream=None):
+    """Appendix D per-tile gaps and Monte Carlo failures.  scores [B,H,T,N_B]
+    fp32 (scores_out layout); tau [B,H] fp32; z [n_samples, N_B] fp32;
+    tiles: device buffer of B*H*T*32 bytes (ugbs_bai_tile records)."""
+    import torch
+    dev = scores.device
+    sc = _check("scores", scores, (p.batch, p.n_heads, p.T, p.NB), (torch.float32,))
+    ns = 0 if z is None else int(z.shape[0])
+    zz = _opt("z", z, (ns, p.NB), (torch.float32,), dev)
+    ta = _opt("tau", tau, (p.batch, p.n_heads), (torch.float32,), dev)
+    tl = _bytes_buf("tiles", tiles, p.batch * p.n_heads * p.T * BAI_TILE_BYTES, dev)
+    _raise("ugbs_bai_tiles", lib().ugbs_bai_tiles(ctypes.byref(p), sc, ta, zz, ns, tl, _stream(stream)))
+
+
+def ugbs_bai_heads(p: Problem, tiles, tau, n_samples, heads, stream=None):
+    """Appendix D per-head aggregates from the tile records; heads: device
+    buffer of B*H*160 bytes (ugbs_bai_head records)."""
+    import torch
+    dev = tau.device
+    ta = _check("tau", tau, (p.batch, p.n_heads), (torch.float32,))
+    tl = _bytes_buf("tiles", tiles, p.batch * p.n_heads * p.T * BAI_TILE_BYTES, dev)
+    hd = _bytes_buf("heads", heads, p.batch * p.n_heads * BAI_HEAD_BYTES, dev)
+    _raise("ugbs_bai_heads", lib().ugbs_bai_heads(ctypes.byref(p), tl, ta, int(n_samples), hd,
+                                                  _stream(stream)))
 
 
 # ---------------------------------------------------------------- convenience

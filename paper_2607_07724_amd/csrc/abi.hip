@@ -131,6 +131,46 @@ int ugbs_route(const ugbs_problem* p, const float* sigma, const int32_t* idx_sor
                                        static_cast<hipStream_t>(stream)));
 }
 
+int ugbs_noise_scale(const ugbs_problem* p, const void* Q, const void* meta, double* rough,
+                     float* tau, void* stream) {
+  Shape s;
+  int st = make_shape(p, &s);
+  if (st) return st;
+  if (!Q || !meta || !rough || !tau) return UGBS_ERR_NULL;
+  if (!aligned(Q, 16) || !aligned(meta, 16) || !aligned(rough, 8) || !aligned(tau, 4))
+    return UGBS_ERR_ALIGN;
+  const hipStream_t hs = static_cast<hipStream_t>(stream);
+  const hipError_t e = ugbs::launch_row_roughness(s, static_cast<const uint16_t*>(Q),
+                                                  static_cast<const uint16_t*>(meta), rough, hs);
+  if (e != hipSuccess) return UGBS_ERR_HIP;
+  return hip_status(ugbs::launch_noise_scale(s, rough, tau, hs));
+}
+
+int ugbs_bai_tiles(const ugbs_problem* p, const float* scores, const float* tau, const float* z,
+                   int32_t n_samples, ugbs_bai_tile* tiles, void* stream) {
+  Shape s;
+  int st = make_shape(p, &s);
+  if (st) return st;
+  if (n_samples < 0 || n_samples > (1 << 20)) return UGBS_ERR_SHAPE;
+  if (!scores || !tiles || (n_samples > 0 && (!tau || !z))) return UGBS_ERR_NULL;
+  if (!aligned(scores, 4) || !aligned(tau, 4) || !aligned(z, 4) || !aligned(tiles, 8))
+    return UGBS_ERR_ALIGN;
+  return hip_status(ugbs::launch_bai_tiles(s, scores, tau, z, n_samples, tiles,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+int ugbs_bai_heads(const ugbs_problem* p, const ugbs_bai_tile* tiles, const float* tau,
+                   int32_t n_samples, ugbs_bai_head* heads, void* stream) {
+  Shape s;
+  int st = make_shape(p, &s);
+  if (st) return st;
+  if (n_samples < 0 || n_samples > (1 << 20)) return UGBS_ERR_SHAPE;
+  if (!tiles || !tau || !heads) return UGBS_ERR_NULL;
+  if (!aligned(tiles, 8) || !aligned(tau, 4) || !aligned(heads, 8)) return UGBS_ERR_ALIGN;
+  return hip_status(ugbs::launch_bai_heads(s, tiles, tau, n_samples, heads,
+                                           static_cast<hipStream_t>(stream)));
+}
+
 int ugbs_attend(const ugbs_problem* p, const void* Q, const void* K, const void* V,
                 const int32_t* kv_idx, int32_t kv_width, void* O, void* stream) {
   Shape s;

@@ -32,7 +32,7 @@
 // across lanes for R <= 128, in LDS above.  sigma uses IEEE fp32 subtract and
 // divide.  Splitting the stages keeps each kernel at its own occupancy (the
 // scoring kernel is bound by registers, the selection kernel by latency).
-#include "ugbs_internal.h"
+#include "select_common.h"
 
 namespace ugbs {
 namespace {
@@ -53,6 +53,7 @@ struct SelParams {
   int32_t* idx_sorted;
   float* sigma;
   float* scratch; // packed candidate scores (workspace), when neither scores_in nor scores_out
+  double* rough;  // per-unit row roughness (diagnostics mode of the score kernel)
   int GW;         // waves (query heads) per workgroup of the score kernel
   int n_groups;   // head groups per kv head = ceil(G / GW)
   int n_wg;       // score-kernel workgroups
@@ -68,37 +69,6 @@ __device__ __forceinline__ size_t packed_row(int bh, int t, int T) {
   const size_t off = (t >= 2) ? (size_t)(t - 1) * (t - 2) / 2 : 0;
   return (size_t)bh * tri + off;
 }
-
-__device__ __forceinline__ uint32_t order_key(float f) {
-  uint32_t u = __float_as_uint(f == 0.0f ? 0.0f : f);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
-__device__ __forceinline__ float key_value(uint32_t k) {
-  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
-}
-
-__device__ __forceinline__ uint4 neg_part(uint4 v) {
-  uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const uint32_t m = ((w[e] >> 15) & 0x00010001u) * 0xffffu;
-    w[e] &= m;
-  }
-  return make_uint4(w[0], w[1], w[2], w[3]);
-}
-
-__device__ __forceinline__ uint4 pos_part(uint4 v) {
-  uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const uint32_t m = ((w[e] >> 15) & 0x00010001u) * 0xffffu;
-    w[e] &= ~m;
-  }
-  return make_uint4(w[0], w[1], w[2], w[3]);
-}
-
-__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 // max over the four 16-lane rows (lanes l, l^16, l^32, l^48) with the gfx950
 // row-swap permutes: permlane32_swap pairs row r with r^2, permlane16_swap
@@ -116,75 +86,6 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) x = min(x, (uint32_t)__shfl_xor((int)x, o));
   return x;
-}
-
-// Largest thr with at least R of the keys held in key[0..nslots) at or above
-// it (0 = empty slot): a most-significant-bit-first radix descent that
-// counts with wave ballots.  *exact: exactly R keys are >= thr.
-template <int S>
-__device__ __forceinline__ uint32_t kth_largest(const uint32_t (&key)[S], int nslots, int R, bool* exact) {
-  uint32_t thr = 0;
-  *exact = false;
-  for (int bit = 31; bit >= 0; --bit) {
-    const uint32_t cand = thr | (1u << bit);
-    int cnt = 0;
-#pragma unroll
-    for (int sl = 0; sl < S; ++sl)
-      if (sl < nslots) cnt += __popcll(__ballot(key[sl] >= cand));
-    if (cnt >= R) {
-      thr = cand;
-      if (cnt == R) {
-        *exact = true;
-        break;
-      }
-    }
-  }
-  return thr;
-}
-
-// R largest of the keys held in key[0..nslots) (0 = empty; entries in
-// position order slot by slot, lane by lane), written to s_sel[0..R) as
-// (key << 32) | ~position, unsorted: the R-th largest key thr comes from
-// kth_largest, then keys above thr and the lowest-position keys equal to
-// thr are compacted.
-template <int S>
-__device__ __forceinline__ void select_top(const uint32_t (&key)[S], const uint32_t (&pos)[S],
-                                           int nslots, int R, uint64_t* s_sel, int lane) {
-  bool exact;
-  const uint32_t thr = kth_largest<S>(key, nslots, R, &exact);
-  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  int base = 0;
-#pragma unroll
-  for (int sl = 0; sl < S; ++sl) {
-    if (sl < nslots) {
-      const bool take = exact ? (key[sl] >= thr) : (key[sl] > thr);
-      const uint64_t mk = __ballot(take);
-      if (take) s_sel[base + __popcll(mk & lt_mask)] = ((uint64_t)key[sl] << 32) | (0xffffffffu - pos[sl]);
-      base += __popcll(mk);
-    }
-  }
-  if (!exact) {
-    int need = R - base;
-#pragma unroll
-    for (int sl = 0; sl < S; ++sl) {
-      if (sl < nslots && need > 0) {
-        const bool eq = key[sl] == thr;
-        const uint64_t mk = __ballot(eq);
-        const int r = __popcll(mk & lt_mask);
-        if (eq && r < need) s_sel[base + r] = ((uint64_t)thr << 32) | (0xffffffffu - pos[sl]);
-        const int took = min(__popcll(mk), need);
-        base += took;
-        need -= took;
-      }
-    }
-  }
-}
-
-// LDS hand-off between lanes of one wave: LDS operations of a wave complete
-// in order, so waiting for this wave's outstanding ones is enough.
-__device__ __forceinline__ void wave_lds_sync() {
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  __builtin_amdgcn_wave_barrier();
 }
 
 // Workgroup barrier without a memory fence (the metadata ring's direct-to-LDS
@@ -254,8 +155,42 @@ __device__ __forceinline__ Group group_of(int id, const SelParams& P) {
   return r;
 }
 
-template <int D, bool QUEST, bool PACKED>
+// What the score kernel produces per unit: the tile-score row (full
+// [.., N_B] layout or a packed workspace row), or, for the noise-scale
+// diagnostic of Appendix D, the sum over candidates and adjacent row pairs
+// of the squared row-to-row score difference.
+enum Out { kOutFull = 0, kOutPacked = 1, kOutRough = 2 };
+
+// Sum over this lane's column of the squared differences between adjacent
+// rows of the 64 x 16 score block.  Lane l holds column l % 16 and rows
+// 16 rt + 4 (l / 16) + i in acc[rt][i]; the successor of a lane's last row
+// in a row tile sits in the next 16-lane group (or, for the last group, in
+// the first group's next row tile).
+__device__ __forceinline__ float row_diff_sq(const f32x4 (&acc)[4], int lane) {
+  const int g = lane >> 4;
+  float nx[4];
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) nx[rt] = __shfl(acc[rt][0], (lane + 16) & 63);
+  float sq = 0.f;
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) {
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+      const float dd = acc[rt][i + 1] - acc[rt][i];
+      sq += dd * dd;
+    }
+    const bool has_next = g < 3 || rt < 3;
+    const float nxt = (g < 3) ? nx[rt] : nx[rt < 3 ? rt + 1 : 3];
+    const float dd = nxt - acc[rt][3];
+    sq += has_next ? dd * dd : 0.f;
+  }
+  return sq;
+}
+
+template <int D, bool QUEST, int OUT>
 __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
+  constexpr bool PACKED = OUT == kOutPacked;
+  constexpr bool ROUGH = OUT == kOutRough;
   using MC = MetaChunk<D, QUEST>;
   constexpr int KD = MC::KD;
   constexpr int KS = KD / 32;
@@ -283,7 +218,9 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
   float* s_row = reinterpret_cast<float*>(smem + P.ring_lds + w * P.row_lds);
 
   // this unit's candidate scores 1..nc: packed rows, or the full [.., N_B] row
-  float* dst = PACKED ? P.scratch + packed_row(gr.b * s.H + h, t, s.T) : P.scores_out + row * s.NB + 1;
+  float* dst = PACKED ? P.scratch + packed_row(gr.b * s.H + h, t, s.T)
+                      : (ROUGH ? nullptr : P.scores_out + row * s.NB + 1);
+  double rough = 0.0;
   if (nc > 0) {
     // ---- A operand: this wave's 64 query rows (Quest: [q- | q+]) ----------
     bf16x8 a[4][KS];
@@ -359,21 +296,34 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
           for (int rt = 0; rt < 4; ++rt)
             acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][ks], b, acc[rt], 0, 0, 0);
         }
-        float mx = acc[0][0];
-#pragma unroll
-        for (int rt = 0; rt < 4; ++rt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, acc[rt][i]);
-        mx = wave_max16(mx);
         const int pos = kChunk * c + c16;
-        if (g == 0 && pos < nc) s_row[pos] = mx;
+        if constexpr (ROUGH) {
+          const float sq = row_diff_sq(acc, lane);
+          rough += (pos < nc) ? (double)sq : 0.0;
+        } else {
+          float mx = acc[0][0];
+#pragma unroll
+          for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) mx = fmaxf(mx, acc[rt][i]);
+          mx = wave_max16(mx);
+          if (g == 0 && pos < nc) s_row[pos] = mx;
+        }
       }
     }
-    if (active) {
+    if (active && !ROUGH) {
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       __builtin_amdgcn_wave_barrier();
       for (int p = lane; p < nc; p += 64) dst[p] = s_row[p];
     }
+  }
+  if constexpr (ROUGH) {
+    if (active) {
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) rough += __shfl_xor(rough, o);
+      if (lane == 0) P.rough[row] = rough;
+    }
+    return;
   }
   if (!active || PACKED) return;
   // full layout: -inf outside C(t) = {1..t-1}
@@ -535,21 +485,7 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
     for (int p = R + lane; p < n2; p += 64) s_sel[p] = 0ull;
     wave_lds_sync();
     // ---- bitonic sort, descending -----------------------------------------
-    for (int size = 2; size <= n2; size <<= 1) {
-      for (int stride = size >> 1; stride > 0; stride >>= 1) {
-        for (int i = lane; i < (n2 >> 1); i += 64) {
-          const int lo = 2 * stride * (i / stride) + (i % stride);
-          const int hi = lo + stride;
-          const uint64_t x = s_sel[lo], y = s_sel[hi];
-          const bool desc = (lo & size) == 0;
-          if (desc ? (x < y) : (x > y)) {
-            s_sel[lo] = y;
-            s_sel[hi] = x;
-          }
-        }
-        wave_lds_sync();
-      }
-    }
+    lds_bitonic_desc(s_sel, n2, lane);
   }
 
   // ---- outputs --------------------------------------------------------------
@@ -578,19 +514,19 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
   }
 }
 
-template <int D, bool QUEST, bool PACKED>
+template <int D, bool QUEST, int OUT>
 hipError_t launch_score(SelParams P, hipStream_t stream) {
   using MC = MetaChunk<D, QUEST>;
   P.ring_lds = kRing * MC::kBytes;
-  P.row_lds = (P.s.NB * 4 + 15) & ~15;
+  P.row_lds = OUT == kOutRough ? 0 : (P.s.NB * 4 + 15) & ~15;
   const size_t smem = (size_t)P.ring_lds + (size_t)P.GW * P.row_lds;
   if (smem > 65536) {
-    const hipError_t e = hipFuncSetAttribute((const void*)score_kernel<D, QUEST, PACKED>,
+    const hipError_t e = hipFuncSetAttribute((const void*)score_kernel<D, QUEST, OUT>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
   }
   const int grid = ((P.n_wg + 7) / 8) * 8;
-  score_kernel<D, QUEST, PACKED><<<grid, 64 * P.GW, smem, stream>>>(P);
+  score_kernel<D, QUEST, OUT><<<grid, 64 * P.GW, smem, stream>>>(P);
   return hipGetLastError();
 }
 
@@ -609,14 +545,25 @@ hipError_t launch_select(const SelParams& P, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <bool PACKED>
+template <int OUT>
 hipError_t launch_score_d(const SelParams& P, hipStream_t stream) {
   const Shape& s = P.s;
   if (s.d == 128)
-    return s.backbone == UGBS_QUEST ? launch_score<128, true, PACKED>(P, stream)
-                                    : launch_score<128, false, PACKED>(P, stream);
-  return s.backbone == UGBS_QUEST ? launch_score<64, true, PACKED>(P, stream)
-                                  : launch_score<64, false, PACKED>(P, stream);
+    return s.backbone == UGBS_QUEST ? launch_score<128, true, OUT>(P, stream)
+                                    : launch_score<128, false, OUT>(P, stream);
+  return s.backbone == UGBS_QUEST ? launch_score<64, true, OUT>(P, stream)
+                                  : launch_score<64, false, OUT>(P, stream);
+}
+
+SelParams score_params(const Shape& s, const uint16_t* Q, const uint16_t* meta) {
+  SelParams P{};
+  P.s = s;
+  P.Q = Q;
+  P.meta = meta;
+  P.GW = s.G < kMaxGroup ? s.G : kMaxGroup;
+  P.n_groups = (s.G + P.GW - 1) / P.GW;
+  P.n_wg = s.B * s.Hkv * s.T * P.n_groups;
+  return P;
 }
 
 }  // namespace
@@ -630,18 +577,12 @@ hipError_t launch_score_select(const Shape& s, const uint16_t* Q, const uint16_t
                                const float* scores_in, float* scores_out,
                                int32_t* idx_sorted, float* sigma, void* workspace,
                                hipStream_t stream) {
-  SelParams P;
-  P.s = s;
-  P.Q = Q;
-  P.meta = meta;
+  SelParams P = score_params(s, Q, meta);
   P.scores_in = scores_in;
   P.scores_out = scores_out;
   P.idx_sorted = idx_sorted;
   P.sigma = sigma;
   P.scratch = static_cast<float*>(workspace);
-  P.GW = s.G < kMaxGroup ? s.G : kMaxGroup;
-  P.n_groups = (s.G + P.GW - 1) / P.GW;
-  P.n_wg = s.B * s.Hkv * s.T * P.n_groups;
   int cap = 2;
   const int rmax = s.W < s.NB ? s.W : s.NB;
   while (cap < rmax) cap <<= 1;
@@ -652,14 +593,21 @@ hipError_t launch_score_select(const Shape& s, const uint16_t* Q, const uint16_t
   P.row_lds = 0;
   if (scores_in) return launch_select<false>(P, stream);
   if (scores_out) {
-    const hipError_t e = launch_score_d<false>(P, stream);
+    const hipError_t e = launch_score_d<kOutFull>(P, stream);
     if (e != hipSuccess) return e;
     P.scores_in = scores_out;
     return launch_select<false>(P, stream);
   }
-  const hipError_t e = launch_score_d<true>(P, stream);
+  const hipError_t e = launch_score_d<kOutPacked>(P, stream);
   if (e != hipSuccess) return e;
   return launch_select<true>(P, stream);
+}
+
+hipError_t launch_row_roughness(const Shape& s, const uint16_t* Q, const uint16_t* meta,
+                                double* rough, hipStream_t stream) {
+  SelParams P = score_params(s, Q, meta);
+  P.rough = rough;
+  return launch_score_d<kOutRough>(P, stream);
 }
 
 }  // namespace ugbs

@@ -35,6 +35,14 @@ size_t score_scratch_bytes(const Shape& s);
 hipError_t launch_route(const Shape& s, int n_pop, int n_trig, const float* sigma,
                         const int32_t* idx_sorted, int32_t* kv_idx, float* sigma_bar,
                         float* tau, uint8_t* trigger, void* workspace, hipStream_t stream);
+// Appendix D diagnostics.
+hipError_t launch_row_roughness(const Shape& s, const uint16_t* Q, const uint16_t* meta,
+                                double* rough, hipStream_t stream);
+hipError_t launch_noise_scale(const Shape& s, const double* rough, float* tau, hipStream_t stream);
+hipError_t launch_bai_tiles(const Shape& s, const float* scores, const float* tau,
+                            const float* z, int n_s, ugbs_bai_tile* tiles, hipStream_t stream);
+hipError_t launch_bai_heads(const Shape& s, const ugbs_bai_tile* tiles, const float* tau, int n_s,
+                            ugbs_bai_head* heads, hipStream_t stream);
 hipError_t launch_attend(const Shape& s, const uint16_t* Q, const uint16_t* K,
                          const uint16_t* V, const int32_t* kv_idx, int kv_width,
                          uint16_t* O, hipStream_t stream);

@@ -230,3 +230,10 @@ def random_kv_idx(seed: int, B: int, H: int, T: int, W: int, shuffle: bool = Tru
                 if junk and len(row) < W:
                     kv[b, h, t, len(row)] = -int(g.integers(1, 5)) if g.random() < 0.5 else T + int(g.integers(1, 50))
     return kv
+
+
+def mc_normals(seed: int, n_samples: int, NB: int) -> np.ndarray:
+    """Standard normal draws z [n_samples, N_B] fp32 for the Monte Carlo of
+    the identification diagnostics (shared by every tile and head)."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 77])))
+    return g.standard_normal((n_samples, NB)).astype(np.float32)

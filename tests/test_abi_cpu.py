@@ -91,6 +91,9 @@ def test_invalid_problem_rejected_by_every_entry_point(kw, code):
     assert L.ugbs_route(ctypes.byref(p), fake, fake, fake, None, None, None, fake, 1 << 20, None) == want
     assert L.ugbs_attend(ctypes.byref(p), fake, fake, fake, fake, 8, fake, None) == want
     assert L.ugbs_workspace_bytes(ctypes.byref(p)) == 0
+    assert L.ugbs_noise_scale(ctypes.byref(p), fake, fake, fake, fake, None) == want
+    assert L.ugbs_bai_tiles(ctypes.byref(p), fake, fake, fake, 4, fake, None) == want
+    assert L.ugbs_bai_heads(ctypes.byref(p), fake, fake, 4, fake, None) == want
 
 
 def test_null_problem_and_null_pointers():
@@ -165,3 +168,73 @@ def test_binding_rejects_host_tensors_before_calling():
         ugbs.ugbs_block_meta(p, K, meta)
     with pytest.raises(ValueError):
         ugbs.ugbs_block_meta(p, K[:, :, :512], meta)
+
+
+def test_header_declares_the_diagnostics():
+    names = _declared()
+    for f in ("ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads"):
+        assert f in names
+
+
+def test_diagnostics_argument_checks():
+    L = ugbs.lib()
+    p = good()
+    fake = ctypes.c_void_p(0x100000)
+    odd4, odd8 = ctypes.c_void_p(0x100002), ctypes.c_void_p(0x100004)
+    ERR_NULL, ERR_ALIGN, ERR_SHAPE = _enum("UGBS_ERR_NULL"), _enum("UGBS_ERR_ALIGN"), _enum("UGBS_ERR_SHAPE")
+    # noise scale: Q, meta, rough, tau required; rough 8-byte aligned
+    for i in range(4):
+        args = [fake] * 4
+        args[i] = None
+        assert L.ugbs_noise_scale(ctypes.byref(p), *args, None) == ERR_NULL
+    assert L.ugbs_noise_scale(ctypes.byref(p), fake, fake, odd8, fake, None) == ERR_ALIGN
+    assert L.ugbs_noise_scale(ctypes.byref(p), ctypes.c_void_p(0x100008), fake, fake, fake, None) == ERR_ALIGN
+    assert L.ugbs_noise_scale(None, fake, fake, fake, fake, None) == ERR_NULL
+    # tiles: tau and z only needed with samples
+    assert L.ugbs_bai_tiles(ctypes.byref(p), None, None, None, 0, fake, None) == ERR_NULL
+    assert L.ugbs_bai_tiles(ctypes.byref(p), fake, None, None, 0, None, None) == ERR_NULL
+    assert L.ugbs_bai_tiles(ctypes.byref(p), fake, None, fake, 8, fake, None) == ERR_NULL
+    assert L.ugbs_bai_tiles(ctypes.byref(p), fake, fake, None, 8, fake, None) == ERR_NULL
+    assert L.ugbs_bai_tiles(ctypes.byref(p), fake, fake, fake, -1, fake, None) == ERR_SHAPE
+    assert L.ugbs_bai_tiles(ctypes.byref(p), fake, fake, fake, (1 << 20) + 1, fake, None) == ERR_SHAPE
+    assert L.ugbs_bai_tiles(ctypes.byref(p), fake, fake, fake, 8, odd8, None) == ERR_ALIGN
+    assert L.ugbs_bai_tiles(ctypes.byref(p), odd4, fake, fake, 8, fake, None) == ERR_ALIGN
+    # heads
+    assert L.ugbs_bai_heads(ctypes.byref(p), None, fake, 4, fake, None) == ERR_NULL
+    assert L.ugbs_bai_heads(ctypes.byref(p), fake, None, 4, fake, None) == ERR_NULL
+    assert L.ugbs_bai_heads(ctypes.byref(p), fake, fake, 4, None, None) == ERR_NULL
+    assert L.ugbs_bai_heads(ctypes.byref(p), fake, fake, -2, fake, None) == ERR_SHAPE
+    assert L.ugbs_bai_heads(ctypes.byref(p), odd8, fake, 4, fake, None) == ERR_ALIGN
+    assert L.ugbs_bai_heads(ctypes.byref(p), fake, fake, 4, odd8, None) == ERR_ALIGN
+
+
+def test_diagnostics_record_layout_matches_header(tmp_path):
+    """Compile a host program against include/ugbs.h and compare sizeof /
+    offsetof of the record structs with the binding's field tables."""
+    import shutil
+    import subprocess
+    import numpy as np
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no host C compiler")
+    tile_fields = [f[0] for f in ugbs.BAI_TILE_FIELDS]
+    head_fields = [f[0] for f in ugbs.BAI_HEAD_FIELDS]
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "ugbs.h"', "int main(void) {",
+             'printf("tile %zu\\n", sizeof(ugbs_bai_tile));',
+             'printf("head %zu\\n", sizeof(ugbs_bai_head));']
+    lines += [f'printf("t.{n} %zu\\n", offsetof(ugbs_bai_tile, {n}));' for n in tile_fields]
+    lines += [f'printf("h.{n} %zu\\n", offsetof(ugbs_bai_head, {n}));' for n in head_fields]
+    lines += ["return 0; }"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = dict(l.split() for l in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                  check=True).stdout.splitlines())
+    td, hd = np.dtype(ugbs.BAI_TILE_FIELDS), np.dtype(ugbs.BAI_HEAD_FIELDS)
+    assert int(out["tile"]) == td.itemsize == ugbs.BAI_TILE_BYTES
+    assert int(out["head"]) == hd.itemsize == ugbs.BAI_HEAD_BYTES
+    for n in tile_fields:
+        assert int(out["t." + n]) == td.fields[n][1], n
+    for n in head_fields:
+        assert int(out["h." + n]) == hd.fields[n][1], n
