@@ -34,7 +34,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="C4", choices=["C2", "C3", "C4"])
+    ap.add_argument("--workload", default=None, choices=["C2", "C3", "C4"])
     ap.add_argument("--q", type=float, default=None)
     ap.add_argument("--cpu-units", type=int, default=3072, help="oracle sample size (tile, head units)")
     ap.add_argument("--no-cpu", action="store_true")
@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache steps")
     ap.add_argument("--stack", action="store_true",
                     help="also time the 28-layer 128K stack (28/4 heads, both backbones) routed vs dense")
+    ap.add_argument("--bai", action="store_true",
+                    help="time the Appendix D diagnostics pass instead (default workload C2)")
+    ap.add_argument("--samples", type=int, default=256, help="Monte Carlo samples of the diagnostics")
     return ap.parse_args()
 
 
@@ -101,11 +104,13 @@ def main():
     import paper_2607_07724_amd as ugbs
     from paper_2607_07724_amd import synth
 
-    w = synth.WORKLOADS[a.workload]
+    w = synth.WORKLOADS[a.workload or ("C2" if a.bai else "C4")]
     if a.q is not None:
         w = w.replace(q=a.q)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if a.bai:
+        return run_bai(a, torch, dev, ugbs, synth, w)
     if a.calibrate_copy:
         # a plain streaming kernel of known size: reads 1 GiB, writes 1 GiB
         src = torch.empty(1 << 29, dtype=torch.int16, device=dev).fill_(1)
@@ -318,6 +323,161 @@ def main():
     if a.json_out:
         with open(a.json_out, "w") as f:
             f.write(line + "\n")
+
+
+BAI_METRIC = "Appendix D diagnostics pass: (batch, head, tile) units per second, 1 MI355X"
+
+
+def run_bai(a, torch, dev, ugbs, synth, w):
+    """One step = the Appendix D diagnostics of one layer: tile scores into
+    HBM (ugbs_score_select with scores_out), row roughness and the noise
+    scale, per-tile gaps with the Monte Carlo over `--samples` shared normal
+    draws, and the per-head aggregates."""
+    log(f"diagnostics workload {w.name}: B={w.B} H={w.H}/{w.Hkv} d={w.d} N={w.N} k={w.k} "
+        f"q={w.q} backbone={w.backbone} samples={a.samples}")
+    inp = synth.generate(w, threads=16)
+
+    def to_dev(x):
+        return torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+
+    Q, K = to_dev(inp.Q), to_dev(inp.K)
+    p = ugbs.Problem.make(w.B, w.H, w.Hkv, w.N, w.d, w.k, w.q, w.backbone)
+    B, H, T, NB = w.B, w.H, w.T, w.NB
+    meta = torch.empty((B, w.Hkv, NB, p.meta_width, w.d), dtype=torch.bfloat16, device=dev)
+    idx = torch.empty((B, H, T, p.W), dtype=torch.int32, device=dev)
+    sig = torch.empty((B, H, T), dtype=torch.float32, device=dev)
+    scores = torch.empty((B, H, T, NB), dtype=torch.float32, device=dev)
+    rough = torch.empty((B, H, T), dtype=torch.float64, device=dev)
+    tau = torch.empty((B, H), dtype=torch.float32, device=dev)
+    z = torch.from_numpy(synth.block_major(synth.mc_normals(w.seed(), a.samples, NB))).to(dev)
+    tiles = torch.empty((B * H * T * ugbs.BAI_TILE_BYTES,), dtype=torch.uint8, device=dev)
+    heads = torch.empty((B * H * ugbs.BAI_HEAD_BYTES,), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    ugbs.ugbs_block_meta(p, K, meta)
+
+    def step(ev=None):
+        rec = (lambda i: ev[i].record(stream)) if ev is not None else (lambda i: None)
+        rec(0)
+        ugbs.ugbs_score_select(p, Q, meta, idx, sig, scores_out=scores)
+        rec(1)
+        ugbs.ugbs_noise_scale(p, Q, meta, rough, tau)
+        rec(2)
+        ugbs.ugbs_bai_tiles(p, scores, tiles, tau=tau, z=z)
+        rec(3)
+        ugbs.ugbs_bai_heads(p, tiles, tau, a.samples, heads)
+        rec(4)
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(a.steps)]
+    t0 = time.perf_counter()
+    for i in range(a.steps):
+        step(evs[i])
+    torch.cuda.synchronize(dev)
+    ms_per_step = 1e3 * (time.perf_counter() - t0) / a.steps
+    st = np.array([[evs[i][j].elapsed_time(evs[i][j + 1]) for j in range(4)] for i in range(a.steps)]).mean(axis=0)
+    log(f"timed {a.steps} steps: {ms_per_step:.3f} ms/step; stages {np.round(st, 4).tolist()}")
+    rec = ugbs.bai_tile_records(tiles).reshape(B, H, T)
+    hd = ugbs.bai_head_records(heads).reshape(B, H)
+    n_valid = int(rec["valid"].sum())
+    # per-unit algorithmic work of the tile kernel: one read of the candidate
+    # scores from HBM, and per (sample, candidate) one fp32 multiply and one add
+    cand = np.array([max(t - 1, 0) for t in range(T)], np.float64)
+    valid_t = rec["valid"][0, 0].astype(bool)
+    bytes_tiles = 4.0 * B * H * cand.sum() + 32.0 * B * H * T
+    flop_mc = 2.0 * a.samples * B * H * cand[valid_t].sum()
+    units = B * H * T
+    tiles_ms = float(st[2])
+    f_rough = flops_scores(B, H, T, w.d, w.backbone)
+    stages = {
+        "score_select_scores_out": {"ms": round(float(st[0]), 4),
+                                    "scores_GBps": round(4.0 * B * H * T * NB / (st[0] * 1e-3) / 1e9, 1)},
+        "noise_scale": {"ms": round(float(st[1]), 4),
+                        "TFLOPs": round(f_rough / (st[1] * 1e-3) / 1e12, 2)},
+        "bai_tiles": {"ms": round(tiles_ms, 4),
+                      "scores_GBps": round(bytes_tiles / (tiles_ms * 1e-3) / 1e9, 1),
+                      "mc_TFLOPs": round(flop_mc / (tiles_ms * 1e-3) / 1e12, 3)},
+        "bai_heads": {"ms": round(float(st[3]), 4)},
+    }
+    dom = int(np.argmax(st))
+    name = ["score_select", "noise_scale", "bai_tiles", "bai_heads"][dom]
+    if name == "bai_tiles":
+        ach = flop_mc / (tiles_ms * 1e-3) / 1e12
+        roof = {"kernel": "bai_tile_kernel", "bound": "alu", "achieved": round(ach, 3),
+                "peak": 157.3, "unit": "TFLOP/s", "frac": round(ach / 157.3, 5), "traffic": None,
+                "flop_per_launch": flop_mc, "note": "fp32 vector peak; 2 flop per (sample, candidate)"}
+    elif name == "noise_scale":
+        ach = f_rough / (st[1] * 1e-3) / 1e12
+        roof = {"kernel": "score_kernel (roughness mode)", "bound": "mfma", "achieved": round(ach, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                "traffic": None, "flop_per_launch": f_rough}
+    else:
+        by = 4.0 * B * H * T * NB
+        ach = by / (st[0] * 1e-3) / 1e9
+        roof = {"kernel": name, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
+    cpu = None if a.no_cpu else cpu_baseline_bai(w, inp, a.samples)
+    out = {
+        "metric": BAI_METRIC,
+        "value": round(units / (ms_per_step * 1e-3), 1),
+        "unit": "units/s",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{w.name} diagnostics: B {B}, {H} q / {w.Hkv} kv heads, d {w.d}, "
+                               f"N {w.N}, k {w.k}, q {w.q}, {a.samples} Monte Carlo samples",
+                   "backbone": "quest" if w.backbone == 1 else "kmean", "seed": w.seed(0)},
+        "stages": stages,
+        "valid_tiles": n_valid,
+        "head0": {f: float(hd[f][0, 0]) for f in ("r_cv", "sigma_q", "tau", "delta2_p05", "chi", "C_q",
+                                                   "bound", "mc_err_k", "mc_err_rk", "mc_regret")},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    line = json.dumps(out)
+    print(line, flush=True)
+    if a.json_out:
+        with open(a.json_out, "w") as f:
+            f.write(line + "\n")
+
+
+def cpu_baseline_bai(w, inp, n_s, kv_heads=2):
+    """The diagnostics oracle on a bounded sample: block metadata, tile
+    scores and row roughness of the query heads of `kv_heads` kv heads,
+    then their tile gaps, Monte Carlo counts and head aggregates; rate in
+    (b, h, t) units/s."""
+    import oracle
+    from oracle import bai
+    threads = min(os.cpu_count() or 1, 16)
+    G = w.H // w.Hkv
+    nh = G * kv_heads
+    Q1 = np.ascontiguousarray(inp.Q[:1, :nh])
+    K1 = np.ascontiguousarray(inp.K[:1, :kv_heads])
+    t0 = time.perf_counter()
+    meta = oracle.block_meta(w.backbone, K1, nthreads=threads)
+    S = oracle.tile_scores(w.backbone, Q1, meta, kv_heads, nthreads=threads)
+    sums, terms = oracle.row_roughness(w.backbone, Q1, meta, kv_heads, nthreads=threads)
+    units = oracle.all_units(1, nh, w.T)
+    tau = np.array([[bai.noise_scale(sums[units[:, 1] == h], terms[units[:, 1] == h])
+                     for h in range(nh)]], np.float32)
+    z = synth_normals(w, n_s)
+    gaps = bai.tile_gaps(S, w.k)
+    fk, fr = bai.mc_counts(S, w.k, tau, z)
+    bai.head_stats(gaps, fk, fr, tau, w.q, w.k, n_s)
+    secs = time.perf_counter() - t0
+    return {"value": round(nh * w.T / secs, 3), "unit": "units/s", "cores": threads, "kind": "oracle",
+            "seconds": round(secs, 2),
+            "sample": f"batch 0, query heads 0..{nh - 1} ({kv_heads} kv heads) of {w.name}: their "
+                      f"{nh * w.T} tiles through metadata, tile scores, row roughness, gaps, "
+                      f"{n_s}-sample Monte Carlo and head aggregates",
+            "host_cpu": _cpu_name()}
+
+
+def synth_normals(w, n_s):
+    from paper_2607_07724_amd import synth
+    return synth.mc_normals(w.seed(), n_s, w.NB)
 
 
 def measured_peaks(torch, dev, stream):

@@ -253,11 +253,12 @@ UGBS_API int ugbs_noise_scale(const ugbs_problem* p, const void* Q, const void* 
  *   scores    : [B, H, T, N_B] fp32 tile scores in the layout of
  *               ugbs_score_select's scores_out (entries of C(t) are read).
  *   tau       : [B, H] fp32 noise scale; may be NULL when n_samples == 0.
- *   z         : [n_samples, N_B] fp32 standard normals shared by all tiles
- *               and heads; may be NULL when n_samples == 0.
+ *   z         : [N_B, n_samples] fp32 standard normals shared by all tiles
+ *               and heads, block-major (draw s of block b at z[b * n_samples
+ *               + s]); may be NULL when n_samples == 0.
  *   n_samples : 0 <= n_samples <= 1 << 20.
  *   tiles     : [B, H, T] ugbs_bai_tile, 8-byte aligned, fully written.
- * For sample s the perturbed scores are mu_b = fp32(c_b + fp32(tau z[s, b]))
+ * For sample s the perturbed scores are mu_b = fp32(c_b + fp32(tau z[b, s]))
  * over b in C(t) (c_b with -0 read as +0).  fail_k counts the samples where
  * NOT (min of mu over the empirical top-m > max of mu over the other
  * candidates); fail_rk the samples where fewer than m members of the

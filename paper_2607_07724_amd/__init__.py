@@ -286,13 +286,14 @@ def ugbs_noise_scale(p: Problem, Q, meta, rough, tau, stream=None):
 
 def ugbs_bai_tiles(p: Problem, scores, tiles, tau=None, z=None, stream=None):
     """Appendix D per-tile gaps and Monte Carlo failures.  scores [B,H,T,N_B]
-    fp32 (scores_out layout); tau [B,H] fp32; z [n_samples, N_B] fp32;
-    tiles: device buffer of B*H*T*32 bytes (ugbs_bai_tile records)."""
+    fp32 (scores_out layout); tau [B,H] fp32; z [N_B, n_samples] fp32
+    (block-major); tiles: device buffer of B*H*T*32 bytes (ugbs_bai_tile
+    records)."""
     import torch
     dev = scores.device
     sc = _check("scores", scores, (p.batch, p.n_heads, p.T, p.NB), (torch.float32,))
-    ns = 0 if z is None else int(z.shape[0])
-    zz = _opt("z", z, (ns, p.NB), (torch.float32,), dev)
+    ns = 0 if z is None else int(z.shape[1])
+    zz = _opt("z", z, (p.NB, ns), (torch.float32,), dev)
     ta = _opt("tau", tau, (p.batch, p.n_heads), (torch.float32,), dev)
     tl = _bytes_buf("tiles", tiles, p.batch * p.n_heads * p.T * BAI_TILE_BYTES, dev)
     _raise("ugbs_bai_tiles", lib().ugbs_bai_tiles(ctypes.byref(p), sc, ta, zz, ns, tl, _stream(stream)))

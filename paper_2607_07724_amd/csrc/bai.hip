@@ -4,9 +4,9 @@
 //                  produces in its roughness mode (recipe step 3: adjacent
 //                  rows of a tile differ by two independent noise draws, so
 //                  the mean squared difference is 2 tau^2).
-// bai_tile_kernel  one wave per (b, h, t): the sorted top rho k - |F| + 1
-//                  candidate scores (same key order as the selection kernel:
-//                  score descending, lower block first), the gaps g, G, r and
+// bai_tile_kernel  per (b, h, t): the sorted top rho k - |F| + 1 candidate
+//                  scores (same key order as the selection kernel: score
+//                  descending, lower block first), the gaps g, G, r and
 //                  sigma of Eq. (gaps), the smallest secondary spacing among
 //                  ranks 0..R' (assumption (A1)), and a Monte Carlo count of
 //                  identification failures of the empirical top-m and top-R'
@@ -19,8 +19,10 @@
 //                  Monte Carlo error rates and regret R_q.
 //
 // Floating-point order: the gaps use fp32 subtract and an IEEE divide; mu is
-// fp32(s + fp32(tau z)) without contraction; the head sums of r run in tile
-// order in fp64, one thread, so they equal a left-to-right sum.
+// fp32(s + fp32(tau z)), a multiply and an add each rounded (the kernels
+// switch floating-point contraction off, so no fused multiply-add); the head
+// sums of r run in tile order in fp64, one thread, so they equal a
+// left-to-right sum.
 #include <math.h>
 
 #include "select_common.h"
@@ -29,7 +31,7 @@ namespace ugbs {
 namespace {
 
 constexpr int kRho = 2;
-constexpr int kBaiWaves = 4;
+constexpr int kBaiUnits = 4;   // query heads of one tile per workgroup (one wave each)
 constexpr int kBaiSlots = UGBS_MAX_BLOCKS / 64;
 constexpr int kHeadThreads = 256;
 
@@ -37,9 +39,13 @@ struct TileParams {
   Shape s;
   const float* scores;  // [B, H, T, N_B]
   const float* tau;     // [B, H]
-  const float* z;       // [n_s, N_B]
+  const float* zT;      // [N_B, n_s]: sample s of block b at zT[b * n_s + s]
   int n_s;
   ugbs_bai_tile* tiles; // [B, H, T]
+  int n_hg;             // head groups per tile, ceil(H / kBaiUnits)
+  int n_wg;             // B * T * n_hg
+  int sel_bytes;        // per-unit LDS: sort buffer, then the masked score row
+  int top_bytes;        // per-unit LDS: the top R' (value, position)
 };
 
 __device__ __forceinline__ float wave_min_f(float x) {
@@ -48,117 +54,204 @@ __device__ __forceinline__ float wave_min_f(float x) {
   return x;
 }
 
-__device__ __forceinline__ float wave_max_f(float x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
-  return x;
-}
-
-__global__ void __launch_bounds__(64 * kBaiWaves) bai_tile_kernel(TileParams P) {
+// One workgroup per (b, t, group of up to 4 query heads): all units share
+// the candidate set C(t) and so every draw z[b', s].
+//
+// Phase 1, wave u = unit u: the sorted top R' + 1 (keys as in the
+// selection kernel), the gaps and the smallest secondary spacing; then, in
+// LDS, the top R' as (value, position) and the unit's score row with the top
+// R' masked to -inf (the candidates outside the expanded set).
+//
+// Phase 2, Monte Carlo with one sample per lane (wave w takes samples w*64 +
+// lane + 256 i): for every unit, mu = fp32(s + fp32(tau z)) is maxed over
+// the masked row (max over the candidates outside the top R'), then the top
+// R' are visited in rank order: the min over ranks < m, the max over ranks
+// m..R'-1, and the count of ranks < R' whose mu beats the outside max.  The
+// draws of a block are read once per workgroup-sample and used by every
+// unit; no cross-lane reduction is needed until the failure counts.
+__global__ void __launch_bounds__(64 * kBaiUnits) bai_tile_kernel(TileParams P) {
 #pragma clang fp contract(off)
   extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int s_fail[kBaiUnits][kBaiUnits][2];
   const Shape& s = P.s;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int n_units = s.B * s.H * s.T;
-  const int n_wg = (n_units + kBaiWaves - 1) / kBaiWaves;
-  const int wg = xcd_remap(blockIdx.x, n_wg);
-  if (wg >= n_wg) return;
-  const int u = wg * kBaiWaves + w;
-  if (u >= n_units) return;
-  const int h = u % s.H;
-  const int rest = u / s.H;
+  const int id = xcd_remap(blockIdx.x, P.n_wg);
+  if (id >= P.n_wg) return;
+  const int hg = id % P.n_hg;
+  const int rest = id / P.n_hg;
   const int t = s.T - 1 - rest % s.T;
   const int b = rest / s.T;
-  const size_t row = ((size_t)b * s.H + h) * s.T + t;
+  const int h0 = hg * kBaiUnits;
+  const int n_act = min(kBaiUnits, s.H - h0);
   const int nf = (t == 0) ? 1 : 2;
   const int nc = (t >= 1) ? t - 1 : 0;
   const int m = s.k - nf;              // kept non-forced slots
   const int Rp = kRho * s.k - nf;      // non-forced slots after expansion
-  ugbs_bai_tile* out = P.tiles + row;
-  if (nc < Rp + 1 || nc <= m) {
-    if (lane == 0) {
+  if (nc < Rp + 1 || nc <= m) {        // outside the diagnostic mask (uniform: depends on t)
+    if (w < n_act && lane == 0) {
       const float nan = __builtin_nanf("");
-      *out = ugbs_bai_tile{nan, nan, nan, nan, nan, 0, 0, 0};
+      P.tiles[((size_t)b * s.H + h0 + w) * s.T + t] = ugbs_bai_tile{nan, nan, nan, nan, nan, 0, 0, 0};
     }
     return;
   }
-  uint64_t* s_sel = reinterpret_cast<uint64_t*>(smem) + (size_t)w * UGBS_MAX_BLOCKS;
-  const float* src = P.scores + row * s.NB + 1;
-  const int nslots = (nc + 63) / 64;
+  auto sel_of = [&](int u) { return smem + (size_t)u * P.sel_bytes; };
+  auto top_of = [&](int u) { return smem + (size_t)kBaiUnits * P.sel_bytes + (size_t)u * P.top_bytes; };
 
-  uint32_t keys[kBaiSlots], pos[kBaiSlots];
-#pragma unroll
-  for (int sl = 0; sl < kBaiSlots; ++sl) {
-    const int p = 64 * sl + lane;
-    keys[sl] = (sl < nslots && p < nc) ? order_key(src[p]) : 0u;
-    pos[sl] = (uint32_t)p;
-  }
-  // sorted top R' + 1 as (key << 32) | ~position, descending
-  const int R1 = Rp + 1;
-  select_top<kBaiSlots>(keys, pos, nslots, R1, s_sel, lane);
-  int n2 = 2;
-  while (n2 < R1) n2 <<= 1;
-  for (int p = R1 + lane; p < n2; p += 64) s_sel[p] = 0ull;
-  wave_lds_sync();
-  lds_bitonic_desc(s_sel, n2, lane);
-
-  auto cs = [&](int j) { return key_value((uint32_t)(s_sel[j] >> 32)); };
-  // smallest secondary spacing: ranks j, j + 1 for j = 0..R'-1 except the cut
-  float d2 = __builtin_huge_valf();
-  for (int j = lane; j < Rp; j += 64)
-    if (j != m - 1) d2 = fminf(d2, cs(j) - cs(j + 1));
-  d2 = wave_min_f(d2);
-
-  // ---- Monte Carlo identification failures -------------------------------
-  const uint64_t thr_k = s_sel[m - 1], thr_r = s_sel[Rp - 1];
-  uint32_t in_k = 0u, in_r = 0u, cand = 0u;
-  float sc[kBaiSlots];
-#pragma unroll
-  for (int sl = 0; sl < kBaiSlots; ++sl) {
-    const int p = 64 * sl + lane;
-    const uint64_t k64 = ((uint64_t)keys[sl] << 32) | (0xffffffffu - (uint32_t)p);
-    const bool c = sl < nslots && p < nc;
-    cand |= (uint32_t)c << sl;
-    in_k |= (uint32_t)(c && k64 >= thr_k) << sl;
-    in_r |= (uint32_t)(c && k64 >= thr_r) << sl;
-    sc[sl] = key_value(keys[sl]);   // the candidate score with -0 read as +0
-  }
-  const float tau = P.n_s > 0 ? P.tau[(size_t)b * s.H + h] : 0.f;
-  int fail_k = 0, fail_rk = 0;
-  for (int smp = 0; smp < P.n_s; ++smp) {
-    const float* zr = P.z + (size_t)smp * s.NB + 1;
-    float mu[kBaiSlots];
-    float mn_k = __builtin_huge_valf(), mx_nk = -__builtin_huge_valf(), mx_nr = -__builtin_huge_valf();
+  // ---- phase 1: order statistics of unit w ---------------------------------
+  float g = 0.f, G = 0.f, r = 0.f, sg = 0.f, d2 = 0.f;
+  if (w < n_act) {
+    const int h = h0 + w;
+    uint64_t* s_sel = reinterpret_cast<uint64_t*>(sel_of(w));
+    const float* src = P.scores + (((size_t)b * s.H + h) * s.T + t) * s.NB + 1;
+    const int nslots = (nc + 63) / 64;
+    uint32_t keys[kBaiSlots], pos[kBaiSlots];
 #pragma unroll
     for (int sl = 0; sl < kBaiSlots; ++sl) {
-      if (sl < nslots) {
-        const int p = 64 * sl + lane;
-        const float zv = zr[p < nc ? p : nc - 1];
-        mu[sl] = __fadd_rn(sc[sl], __fmul_rn(tau, zv));
-        if ((cand >> sl) & 1u) {
-          if ((in_k >> sl) & 1u) mn_k = fminf(mn_k, mu[sl]);
-          else mx_nk = fmaxf(mx_nk, mu[sl]);
-          if (!((in_r >> sl) & 1u)) mx_nr = fmaxf(mx_nr, mu[sl]);
+      const int p = 64 * sl + lane;
+      keys[sl] = (sl < nslots && p < nc) ? order_key(src[p]) : 0u;
+      pos[sl] = (uint32_t)p;
+    }
+    // sorted top R' + 1 as (key << 32) | ~position, descending
+    const int R1 = Rp + 1;
+    select_top<kBaiSlots>(keys, pos, nslots, R1, s_sel, lane);
+    int n2 = 2;
+    while (n2 < R1) n2 <<= 1;
+    for (int p = R1 + lane; p < n2; p += 64) s_sel[p] = 0ull;
+    wave_lds_sync();
+    lds_bitonic_desc(s_sel, n2, lane);
+
+    auto cs = [&](int j) { return key_value((uint32_t)(s_sel[j] >> 32)); };
+    // smallest secondary spacing: ranks j, j + 1 for j = 0..R'-1 except the cut
+    float dm = __builtin_huge_valf();
+    for (int j = lane; j < Rp; j += 64)
+      if (j != m - 1) dm = fminf(dm, cs(j) - cs(j + 1));
+    d2 = wave_min_f(dm);
+    {
+      const float c0 = cs(0), cm1 = cs(m - 1), cm = cs(m), cR = cs(Rp);
+      g = cm1 - cm;
+      G = cm1 - cR;
+      r = c0 - cm;
+      sg = (r == 0.0f) ? 0.0f : __fdiv_rn(g, r);
+    }
+    // the top R' in rank order, and the row with them masked out
+    float* tv = reinterpret_cast<float*>(top_of(w));
+    int32_t* tp = reinterpret_cast<int32_t*>(tv + Rp);
+    for (int j = lane; j < Rp; j += 64) {
+      const uint64_t e = s_sel[j];
+      tv[j] = key_value((uint32_t)(e >> 32));
+      tp[j] = (int32_t)(0xffffffffu - (uint32_t)e);
+    }
+    const uint64_t thr_r = s_sel[Rp - 1];
+    wave_lds_sync();  // every read of the sort buffer is done before the row overwrites it
+    float* row = reinterpret_cast<float*>(s_sel);
+#pragma unroll
+    for (int sl = 0; sl < kBaiSlots; ++sl) {
+      const int p = 64 * sl + lane;
+      if (sl < nslots && p < nc) {
+        const uint64_t k64 = ((uint64_t)keys[sl] << 32) | (0xffffffffu - (uint32_t)p);
+        row[p] = (k64 >= thr_r) ? -__builtin_huge_valf() : key_value(keys[sl]);
+      }
+    }
+    const int nc8 = (nc + 7) & ~7;
+    if (lane < nc8 - nc) row[nc + lane] = -__builtin_huge_valf();
+  }
+  __syncthreads();
+
+  // ---- phase 2: Monte Carlo, one sample per lane ---------------------------
+  float tau_u[kBaiUnits];
+#pragma unroll
+  for (int u = 0; u < kBaiUnits; ++u)
+    tau_u[u] = (u < n_act && P.n_s > 0) ? P.tau[(size_t)b * s.H + h0 + u] : 0.f;  // tau may be NULL without samples
+  int fk_acc[kBaiUnits] = {0, 0, 0, 0}, fr_acc[kBaiUnits] = {0, 0, 0, 0};
+  const int nc8 = (nc + 7) & ~7;
+  const size_t ns = (size_t)P.n_s;
+  for (int s0 = 64 * w; s0 < P.n_s; s0 += 64 * kBaiUnits) {
+    const int smp = s0 + lane;
+    const bool live = smp < P.n_s;
+    // draw of block b' for this lane's sample: (zT + b' n_s)[smp_c], with the
+    // block offset uniform (scalar base) and the sample offset per lane
+    const int smp_c = live ? smp : P.n_s - 1;
+    auto zdraw = [&](int blk) { return (P.zT + (size_t)blk * ns)[smp_c]; };
+    float mx_out[kBaiUnits];
+#pragma unroll
+    for (int u = 0; u < kBaiUnits; ++u) mx_out[u] = -__builtin_huge_valf();
+    // candidates outside the top R' (the masked row: the top R' and the
+    // padding read -inf, which no draw changes); the next 8 draws are in
+    // flight while the current 8 are used
+    float zn[8];
+    auto load8 = [&](int p0, float (&zz)[8]) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) zz[i] = zdraw(min(1 + p0 + i, s.NB - 1));
+    };
+    load8(0, zn);
+    for (int p = 0; p < nc8; p += 8) {
+      float zz[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) zz[i] = zn[i];
+      if (p + 8 < nc8) load8(p + 8, zn);
+#pragma unroll
+      for (int u = 0; u < kBaiUnits; ++u) {
+        if (u < n_act) {
+          const float* rw = reinterpret_cast<const float*>(sel_of(u)) + p;
+          const float4 ra = *reinterpret_cast<const float4*>(rw);
+          const float4 rb = *reinterpret_cast<const float4*>(rw + 4);
+          const float rv[8] = {ra.x, ra.y, ra.z, ra.w, rb.x, rb.y, rb.z, rb.w};
+          float mx = mx_out[u];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) mx = fmaxf(mx, rv[i] + tau_u[u] * zz[i]);
+          mx_out[u] = mx;
         }
       }
     }
-    mn_k = wave_min_f(mn_k);
-    mx_nk = wave_max_f(mx_nk);
-    mx_nr = wave_max_f(mx_nr);
-    int above = 0;
+    // the top R' in rank order, 8 draws at a time: ranks < m (min, and the
+    // count above the outside max), then ranks m..R'-1 (max, and the count)
 #pragma unroll
-    for (int sl = 0; sl < kBaiSlots; ++sl)
-      if (sl < nslots) above += __popcll(__ballot(((in_r >> sl) & 1u) && mu[sl] > mx_nr));
-    fail_k += !(mn_k > mx_nk);
-    fail_rk += above < m;
+    for (int u = 0; u < kBaiUnits; ++u) {
+      if (u < n_act) {
+        const float* tv = reinterpret_cast<const float*>(top_of(u));
+        const int32_t* tp = reinterpret_cast<const int32_t*>(tv + Rp);
+        const float tu = tau_u[u], mo = mx_out[u];
+        float mn_in = __builtin_huge_valf(), mx_mid = -__builtin_huge_valf();
+        int above = 0;
+        for (int j0 = 0; j0 < Rp; j0 += 8) {
+          float zz[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+            zz[i] = zdraw(1 + __builtin_amdgcn_readfirstlane(tp[min(j0 + i, Rp - 1)]));
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const int j = j0 + i;
+            if (j < Rp) {
+              const float x = tv[j] + tu * zz[i];
+              if (j < m) mn_in = fminf(mn_in, x);
+              else mx_mid = fmaxf(mx_mid, x);
+              above += x > mo;
+            }
+          }
+        }
+        const bool fail_k = !(mn_in > fmaxf(mx_mid, mo));
+        const bool fail_rk = above < m;
+        fk_acc[u] += __popcll(__ballot(live && fail_k));
+        fr_acc[u] += __popcll(__ballot(live && fail_rk));
+      }
+    }
   }
-
   if (lane == 0) {
-    const float c0 = cs(0), cm1 = cs(m - 1), cm = cs(m), cR = cs(Rp);
-    const float g = cm1 - cm, G = cm1 - cR, r = c0 - cm;
-    const float sg = (r == 0.0f) ? 0.0f : __fdiv_rn(g, r);
-    *out = ugbs_bai_tile{g, G, r, sg, d2, fail_k, fail_rk, 1};
+#pragma unroll
+    for (int u = 0; u < kBaiUnits; ++u) {
+      s_fail[w][u][0] = fk_acc[u];
+      s_fail[w][u][1] = fr_acc[u];
+    }
+  }
+  __syncthreads();
+  if (w < n_act && lane == 0) {
+    int fk = 0, fr = 0;
+    for (int v = 0; v < kBaiUnits; ++v) {
+      fk += s_fail[v][w][0];
+      fr += s_fail[v][w][1];
+    }
+    P.tiles[((size_t)b * s.H + h0 + w) * s.T + t] = ugbs_bai_tile{g, G, r, sg, d2, fk, fr, 1};
   }
 }
 
@@ -406,18 +499,33 @@ hipError_t launch_noise_scale(const Shape& s, const double* rough, float* tau, h
 }
 
 hipError_t launch_bai_tiles(const Shape& s, const float* scores, const float* tau,
-                            const float* z, int n_s, ugbs_bai_tile* tiles, hipStream_t stream) {
-  TileParams P{s, scores, tau, z, n_s, tiles};
-  const size_t smem = (size_t)kBaiWaves * UGBS_MAX_BLOCKS * sizeof(uint64_t);
+                            const float* zT, int n_s, ugbs_bai_tile* tiles, hipStream_t stream) {
+  TileParams P{};
+  P.s = s;
+  P.scores = scores;
+  P.tau = tau;
+  P.zT = zT;
+  P.n_s = n_s;
+  P.tiles = tiles;
+  P.n_hg = (s.H + kBaiUnits - 1) / kBaiUnits;
+  P.n_wg = s.B * s.T * P.n_hg;
+  // sort buffer for the top R' + 1 (a power of two of 8-byte entries; only
+  // tiles with R' + 1 <= |C(t)| <= N_B - 2 are sorted), reused for the
+  // masked score row (N_B floats, padded to a multiple of 8)
+  const int r1 = kRho * s.k - 1;
+  int n2 = 2;
+  while (n2 < r1 && n2 < s.NB) n2 <<= 1;
+  const int sel = 8 * n2 > 4 * (s.NB + 8) ? 8 * n2 : 4 * (s.NB + 8);
+  P.sel_bytes = (sel + 15) & ~15;
+  P.top_bytes = (8 * (kRho * s.k) + 15) & ~15;
+  const size_t smem = (size_t)kBaiUnits * (P.sel_bytes + P.top_bytes);
   if (smem > 65536) {
     const hipError_t e = hipFuncSetAttribute((const void*)bai_tile_kernel,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
   }
-  const int n_units = s.B * s.H * s.T;
-  const int n_wg = (n_units + kBaiWaves - 1) / kBaiWaves;
-  const int grid = ((n_wg + 7) / 8) * 8;
-  bai_tile_kernel<<<grid, 64 * kBaiWaves, smem, stream>>>(P);
+  const int grid = ((P.n_wg + 7) / 8) * 8;
+  bai_tile_kernel<<<grid, 64 * kBaiUnits, smem, stream>>>(P);
   return hipGetLastError();
 }
 

@@ -234,6 +234,12 @@ def random_kv_idx(seed: int, B: int, H: int, T: int, W: int, shuffle: bool = Tru
 
 def mc_normals(seed: int, n_samples: int, NB: int) -> np.ndarray:
     """Standard normal draws z [n_samples, N_B] fp32 for the Monte Carlo of
-    the identification diagnostics (shared by every tile and head)."""
+    the identification diagnostics (shared by every tile and head); the
+    device entry point takes the block-major transpose, see block_major."""
     g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 77])))
     return g.standard_normal((n_samples, NB)).astype(np.float32)
+
+
+def block_major(z: np.ndarray) -> np.ndarray:
+    """z [n_samples, N_B] -> [N_B, n_samples], contiguous."""
+    return np.ascontiguousarray(np.asarray(z, np.float32).T)

@@ -259,3 +259,24 @@ def test_row_roughness_closed_form(backbone):
         assert terms[u] == 63 * max(t - 1, 0)
     tau = bai.noise_scale(sums[units[:, 1] == 0], terms[units[:, 1] == 0])
     assert tau >= 0
+
+
+def test_mc_mu_rounds_product_and_sum_separately():
+    """mu = fp32(s + fp32(tau z)): the product is rounded before the add.
+    For tau = 0.8647483, z = 0.7718125, s = 0.8033179 the exact value lies
+    within half an ulp of 1.4707414 but the twice-rounded one is 1.4707415,
+    equal to the kept block's score: a tie, hence an identification failure
+    (the kept set must beat every other candidate strictly)."""
+    from fractions import Fraction
+    f32 = np.float32
+    tau, zx, cx = f32(0.8647483), f32(0.7718125), f32(0.8033179)
+    exact = Fraction(float(cx)) + Fraction(float(tau)) * Fraction(float(zx))
+    one = f32(1.4707414)
+    up = np.nextafter(one, f32(2))
+    assert abs(exact - Fraction(float(one))) < abs(exact - Fraction(float(up)))  # single rounding: 1.4707414
+    S = np.full((1, 1, 8, 8), -np.inf, f32)
+    S[0, 0, 6, 1:6] = [up, cx, f32(0.1), f32(0.05), f32(0.0)]
+    z = np.zeros((1, 8), f32)
+    z[0, 2] = zx
+    fk, fr = bai.mc_counts(S, 3, np.array([[tau]], f32), z)
+    assert fk[0, 0, 6] == 1 and fr[0, 0, 6] == 0

@@ -84,7 +84,7 @@ def gpu_tiles(p, S, tau32, z):
     tiles = torch.empty((p.batch * p.n_heads * p.T * ugbs.BAI_TILE_BYTES,), dtype=torch.uint8,
                         device="cuda")
     ugbs.ugbs_bai_tiles(p, dev(S), tiles, tau=dev(tau32) if tau32 is not None else None,
-                        z=dev(z) if z is not None else None)
+                        z=dev(synth.block_major(z)) if z is not None else None)
     torch.cuda.synchronize()
     return tiles, ugbs.bai_tile_records(tiles).reshape(p.batch, p.n_heads, p.T)
 
@@ -325,9 +325,135 @@ def test_chain_on_scores_out_matches_selection_sigma(name):
     so = torch.empty((w.B, w.H, w.T, w.NB), dtype=torch.float32, device="cuda")
     ugbs.ugbs_score_select(p, Q, meta, idx, sig, scores_out=so)
     tiles = torch.empty((w.B * w.H * w.T * ugbs.BAI_TILE_BYTES,), dtype=torch.uint8, device="cuda")
-    ugbs.ugbs_bai_tiles(p, so, tiles, tau=dev(c["tau32"]), z=dev(c["z"]))
+    ugbs.ugbs_bai_tiles(p, so, tiles, tau=dev(c["tau32"]), z=dev(synth.block_major(c["z"])))
     torch.cuda.synchronize()
     rec = ugbs.bai_tile_records(tiles).reshape(w.B, w.H, w.T)
     v = rec["valid"].astype(bool)
     assert np.array_equal(v, bai.tile_gaps(c["S"], w.k)["valid"])
     assert np.array_equal(rec["sigma"][v].view(np.uint32), host(sig)[v].view(np.uint32))
+
+
+# ---------------------------------------------------------------- full size
+
+def _unit_oracle(S_row, t, NB, k, tau, z):
+    """Oracle gaps and MC counts of one unit: its score row placed as the
+    last tile of a [1, 1, t + 1, N_B] array."""
+    S = np.full((1, 1, t + 1, NB), -np.inf, np.float32)
+    S[0, 0, t] = S_row
+    g = bai.tile_gaps(S, k)
+    fk, fr = bai.mc_counts(S, k, np.array([[tau]], np.float32), z)
+    return {f: g[f][0, 0, t] for f in g}, int(fk[0, 0, t]), int(fr[0, 0, t])
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["C2", "C3"])
+def test_full_size_diagnostics(name):
+    """The whole diagnostics pass at 32K / 64K in the benchmark's launch
+    configuration: sampled units against the oracle (tiles given the
+    oracle's scores, roughness from the same inputs), and properties of the
+    per-head aggregates that hold at any size."""
+    torch = __import__("torch")
+    w = synth.WORKLOADS[name]
+    inp = synth.generate(w, threads=16)
+    p = problem(w)
+    B, H, T, NB = w.B, w.H, w.T, w.NB
+    Q, K = dev_bf16(inp.Q), dev_bf16(inp.K)
+    meta = torch.empty((B, w.Hkv, NB, p.meta_width, w.d), dtype=torch.bfloat16, device="cuda")
+    ugbs.ugbs_block_meta(p, K, meta)
+    idx = torch.empty((B, H, T, p.W), dtype=torch.int32, device="cuda")
+    sig = torch.empty((B, H, T), dtype=torch.float32, device="cuda")
+    so = torch.empty((B, H, T, NB), dtype=torch.float32, device="cuda")
+    ugbs.ugbs_score_select(p, Q, meta, idx, sig, scores_out=so)
+    rough = torch.empty((B, H, T), dtype=torch.float64, device="cuda")
+    tau = torch.empty((B, H), dtype=torch.float32, device="cuda")
+    ugbs.ugbs_noise_scale(p, Q, meta, rough, tau)
+    n_s = 128
+    z = synth.mc_normals(w.seed(), n_s, NB)
+    zd = dev(synth.block_major(z))
+    tiles = torch.empty((B * H * T * ugbs.BAI_TILE_BYTES,), dtype=torch.uint8, device="cuda")
+    ugbs.ugbs_bai_tiles(p, so, tiles, tau=tau, z=zd)
+    heads = torch.empty((B * H * ugbs.BAI_HEAD_BYTES,), dtype=torch.uint8, device="cuda")
+    ugbs.ugbs_bai_heads(p, tiles, tau, n_s, heads)
+    torch.cuda.synchronize()
+
+    # ---- sampled units: roughness against the oracle on the same inputs
+    g = np.random.default_rng(w.seed())
+    ts = sorted({2, 2 * w.k - 1, 2 * w.k, T - 1} | set(int(x) for x in g.integers(2, T, 8)))
+    units = np.array([(0, int(g.integers(0, H)), t) for t in ts], np.int32)
+    meta_np = oracle.block_meta(w.backbone, inp.K, nthreads=16)
+    sums, _ = oracle.row_roughness(w.backbone, inp.Q, meta_np, w.Hkv, units=units, nthreads=16)
+    rg = host(rough)
+    for i, (b, h, t) in enumerate(units):
+        assert abs(rg[b, h, t] - sums[i]) <= 1e-4 * sums[i], (b, h, t)
+    # tau is the stated function of the roughness sums
+    terms = 63.0 * (T - 1) * (T - 2) / 2
+    assert np.allclose(host(tau), np.sqrt(rg.sum(axis=2) / (2 * terms)).astype(np.float32), rtol=1e-6)
+
+    # ---- sampled tiles given the oracle's scores: bit-exact
+    S = oracle.tile_scores(w.backbone, inp.Q, meta_np, w.Hkv, units=units, nthreads=16)
+    sin = torch.full((B, H, T, NB), -np.inf, dtype=torch.float32, device="cuda")
+    for i, (b, h, t) in enumerate(units):
+        sin[b, h, t] = torch.from_numpy(S[i]).cuda()
+    tau_in = np.full((B, H), 0.05, np.float32)
+    t2 = torch.empty_like(tiles)
+    ugbs.ugbs_bai_tiles(p, sin, t2, tau=dev(tau_in), z=zd)
+    torch.cuda.synchronize()
+    rec = ugbs.bai_tile_records(t2).reshape(B, H, T)
+    for i, (b, h, t) in enumerate(units):
+        ref, fk, fr = _unit_oracle(S[i], int(t), NB, w.k, float(tau_in[b, h]), z)
+        r = rec[b, h, t]
+        assert bool(r["valid"]) == bool(ref["valid"]), (b, h, t)
+        for f in ("g", "G", "r", "sigma", "delta2"):
+            assert same_f32(r[f], ref[f]), (f, b, h, t)
+        assert (int(r["fail_k"]), int(r["fail_rk"])) == (fk, fr), (b, h, t)
+    del sin, t2
+
+    # ---- the GPU chain: properties of tiles and heads at full size
+    rec = ugbs.bai_tile_records(tiles).reshape(B, H, T)
+    hd = ugbs.bai_head_records(heads).reshape(B, H)
+    v = rec["valid"].astype(bool)
+    t_idx = np.arange(T)
+    assert np.array_equal(v, np.broadcast_to(t_idx >= 2 * w.k, v.shape))
+    sg = host(sig)
+    assert np.array_equal(rec["sigma"][v].view(np.uint32), sg[v].view(np.uint32))
+    assert (rec["fail_k"] >= rec["fail_rk"]).all()
+    n = T - 2 * w.k
+    nq = math.ceil(w.q * n)
+    for b in range(B):
+        for h in range(H):
+            x = hd[b, h]
+            s_h = rec["sigma"][b, h][v[b, h]]
+            d_h = rec["delta2"][b, h][v[b, h]]
+            assert x["n_tiles"] == n and x["n_q"] == nq
+            assert (s_h < x["sigma_q"]).sum() < nq <= (s_h <= x["sigma_q"]).sum()
+            assert x["pi2"] == (d_h < x["delta2_p05"]).sum() / n
+            assert x["delta2_p05"] == np.sort(d_h)[int(math.floor(0.05 * (n - 1)))]
+            assert x["mc_err_rk"] <= x["mc_err_k"] and x["mc_regret"] >= 0
+            assert x["C_q"] <= 1.0 and x["bound"] <= min(w.q, 1 - w.q) + x["pi2"] + 1e-15
+            assert x["tau"] == float(host(tau)[b, h])
+
+
+def test_mc_mu_is_rounded_twice():
+    """mu = fp32(s + fp32(tau z)) with both roundings: a tile built so that a
+    fused multiply-add would change one comparison.  With tau = 0.8647483,
+    z = 0.7718125 and s = 0.8033179, the two roundings give 1.4707415 and a
+    single rounding 1.4707414; the kept block's mu is exactly 1.4707415, so
+    the outside block ties it (a failure) only under double rounding."""
+    f32 = np.float32
+    T = 8
+    tau, zx, cx = f32(0.8647483), f32(0.7718125), f32(0.8033179)
+    mu_x = f32(cx + f32(tau * zx))
+    assert mu_x == f32(1.4707415)
+    S = np.full((1, 1, T, T), -np.inf, f32)
+    g = np.random.default_rng(3)
+    for t in range(2, T):
+        S[0, 0, t, 1:t] = g.uniform(-1, 0, t - 1).astype(f32)
+    # tile 6, k = 3: m = 1 kept, R' = 4; block 1 is the kept one, block 2 the runner-up
+    S[0, 0, 6, 1:6] = [mu_x, cx, f32(0.1), f32(0.05), f32(0.0)]
+    z = np.zeros((1, T), f32)
+    z[0, 2] = zx
+    p = ugbs.Problem.make(1, 1, 1, 64 * T, 64, 3, 0.5)
+    tau32 = np.array([[tau]], f32)
+    _, rec = gpu_tiles(p, S, tau32, z)
+    check_tiles(rec, S, 3, tau32, z)
+    assert rec["fail_k"][0, 0, 6] == 1 and rec["fail_rk"][0, 0, 6] == 0
