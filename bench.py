@@ -169,6 +169,40 @@ def main():
     step_ms = np.array([evs[i][0].elapsed_time(evs[i][4]) for i in range(a.steps)])
     log(f"timed {a.steps} steps: {ms_per_step:.3f} ms/step; stages {np.round(stage_avg, 4).tolist()}")
 
+    # the same layer with the selection inside the attention kernel (no kv_idx lists)
+    fb = ugbs.Buffers(p, device=dev)
+    Of = torch.empty_like(Q)
+
+    def step_fused(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        ugbs.ugbs_block_meta(p, K, fb.meta)
+        if ev is not None:
+            ev[1].record(stream)
+        ugbs.ugbs_score_select(p, Q, fb.meta, None, fb.sigma, workspace=fb.workspace)
+        if ev is not None:
+            ev[2].record(stream)
+        ugbs.ugbs_route(p, fb.sigma, None, None, fb.workspace, fb.sigma_bar, fb.tau, fb.trigger)
+        if ev is not None:
+            ev[3].record(stream)
+        ugbs.ugbs_attend_select(p, Q, K, V, Of, workspace=fb.workspace)
+        if ev is not None:
+            ev[4].record(stream)
+
+    for i in range(a.warmup):
+        step_fused()
+    torch.cuda.synchronize(dev)
+    fevs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(a.steps)]
+    t0 = time.perf_counter()
+    for i in range(a.steps):
+        step_fused(fevs[i])
+    torch.cuda.synchronize(dev)
+    fused_ms = 1e3 * (time.perf_counter() - t0) / a.steps
+    fst = np.array([[fevs[i][j].elapsed_time(fevs[i][j + 1]) for j in range(4)] for i in range(a.steps)]).mean(axis=0)
+    same = bool(torch.equal(O.view(torch.int16), Of.view(torch.int16)))
+    log(f"fused: {fused_ms:.3f} ms/step; stages {np.round(fst, 4).tolist()}; output identical: {same}")
+    del fb
+
     cold = None
     if not a.no_cold:
         # caches cold: a 1 GiB write (twice the 256 MB last-level cache) before each single step
@@ -311,6 +345,13 @@ def main():
         "selection": {"mean_kept_blocks": round(float(kept.mean()), 3),
                       "triggered_tiles": int(trig.sum()),
                       "needle_hit_rate": hit_rate},
+        "fused_selection": {"ms_per_step": round(fused_ms, 4),
+                            "stages_ms": {"block_meta": round(float(fst[0]), 4),
+                                          "score_sigma": round(float(fst[1]), 4),
+                                          "route_flags": round(float(fst[2]), 4),
+                                          "attend_select": round(float(fst[3]), 4)},
+                            "attend_select_TFLOPs": round(f_att / (fst[3] * 1e-3) / 1e12, 2),
+                            "output_identical": same},
         "ms_per_step_median": round(float(np.median(step_ms)), 4),
         "cold": cold,
         "measured_peaks": probe,

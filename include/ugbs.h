@@ -16,6 +16,11 @@
  *   ugbs_score_select (Q, meta, workspace)   -> idx_sorted, sigma
  *   ugbs_route        (sigma, idx_sorted)    -> kv_idx (may alias idx_sorted)
  *   ugbs_attend       (Q, K, V, kv_idx)      -> O
+ * or, with the selection inside the attention kernel (no kv_idx lists):
+ *   ugbs_block_meta   (K)                    -> meta
+ *   ugbs_score_select (Q, meta, workspace)   -> sigma (idx_sorted NULL)
+ *   ugbs_route        (sigma, workspace)     -> trigger flags (kv_idx NULL)
+ *   ugbs_attend_select(Q, K, V, workspace)   -> O
  * No call synchronises the device; none allocates device memory.
  *
  * Diagnostics (Appendix D: sigma as a best-arm identification index), off
@@ -57,7 +62,7 @@ extern "C" {
 #define UGBS_API
 #endif
 
-#define UGBS_ABI_VERSION 3
+#define UGBS_ABI_VERSION 4
 #define UGBS_BLOCK 64          /* BLOCK_M = BLOCK_N = 64 tokens (Section 3.1, 3.2) */
 #define UGBS_MAX_BLOCKS 2048   /* N_B <= 2048, i.e. N <= 131072 */
 #define UGBS_MAX_KV_WIDTH 4096 /* kv_width accepted by ugbs_attend; k_budget <= 2048 */
@@ -121,21 +126,23 @@ UGBS_API int ugbs_block_meta(const ugbs_problem* p, const void* K, void* meta, v
  *                computed ones (only entries in C(t) are read).
  *   scores_out : NULL, or [B, H, T, N_B] fp32; receives the tile scores,
  *                -inf outside C(t).
- *   idx_sorted : [B, H, T, 2k] int32.  Row (t, h) is [0] (t = 0) or [0, t],
- *                then C(t) ordered by score descending, lower block index
- *                first on equal scores (-0 == +0), cut at 2k slots and
- *                padded with the sentinel N_B.
+ *   idx_sorted : [B, H, T, 2k] int32, or NULL (sigma only).  Row (t, h) is
+ *                [0] (t = 0) or [0, t], then C(t) ordered by score
+ *                descending, lower block index first on equal scores
+ *                (-0 == +0), cut at 2k slots and padded with the sentinel
+ *                N_B.
  *   sigma      : [B, H, T] fp32.  With F the forced list and m = k - |F|:
  *                sigma = (c[m-1] - c[m]) / (c[0] - c[m]) over the sorted
  *                candidate scores c (fp32 arithmetic), 0 when the
  *                denominator is 0, and -1 when |C(t)| <= m (a saturated
  *                tile: it keeps every visible block).
  *   workspace  : needed only when scores_in and scores_out are both NULL
- *                (the tile scores then pass through it): device memory of
- *                at least ugbs_workspace_bytes(p) bytes, 256-byte aligned,
- *                owned by the caller, contents on entry ignored; otherwise
- *                may be NULL.  Two calls that overlap in time must not share
- *                a workspace.
+ *                (the tile scores then pass through it, and stay there for
+ *                ugbs_attend_select): device memory of at least
+ *                ugbs_workspace_bytes(p) bytes, 256-byte aligned, owned by
+ *                the caller, contents on entry ignored; otherwise may be
+ *                NULL.  Two calls that overlap in time must not share a
+ *                workspace.
  *   Q and meta are read-only; idx_sorted/sigma/scores_out are fully written. */
 UGBS_API int ugbs_score_select(const ugbs_problem* p, const void* Q, const void* meta,
                       const float* scores_in, float* scores_out,
@@ -153,16 +160,19 @@ UGBS_API int ugbs_score_select(const ugbs_problem* p, const void* Q, const void*
  *   trigger).  kv_idx = idx_sorted, with slots k..2k-1 of every row of a
  *   tile that does not trigger overwritten by the sentinel N_B.
  *   sigma      : [B, H, T] fp32 from ugbs_score_select.
- *   idx_sorted : [B, H, T, 2k] int32.
+ *   idx_sorted : [B, H, T, 2k] int32, or NULL together with kv_idx (then
+ *                only the statistics and trigger flags are produced).
  *   kv_idx     : [B, H, T, 2k] int32; may equal idx_sorted (in place: only
  *                the sentinel slots are written).
  *   sigma_bar  : NULL or [B, T] fp32 (-1 outside P).
  *   tau        : NULL or [B] fp32 (-1 when no tile triggers).
  *   trigger    : NULL or [B, T] uint8 (0/1).
  *   workspace  : device memory of at least ugbs_workspace_bytes(p) bytes,
- *                256-byte aligned, owned by the caller; its contents on entry
- *                are ignored.  Two calls that overlap in time must not share
- *                a workspace. */
+ *                256-byte aligned, owned by the caller.  The route's own
+ *                sections are overwritten (the trigger flags stay there for
+ *                ugbs_attend_select); the packed tile scores that
+ *                ugbs_score_select left there are not touched.  Two calls
+ *                that overlap in time must not share a workspace. */
 UGBS_API int ugbs_route(const ugbs_problem* p, const float* sigma, const int32_t* idx_sorted,
                int32_t* kv_idx, float* sigma_bar, float* tau, uint8_t* trigger,
                void* workspace, size_t workspace_bytes, void* stream);
@@ -275,10 +285,34 @@ UGBS_API int ugbs_bai_tiles(const ugbs_problem* p, const float* scores, const fl
 UGBS_API int ugbs_bai_heads(const ugbs_problem* p, const ugbs_bai_tile* tiles, const float* tau,
                             int32_t n_samples, ugbs_bai_head* heads, void* stream);
 
-/* Bytes of device workspace ugbs_score_select (without scores_in/scores_out)
- * and ugbs_route need for problem p; one workspace serves both calls in
- * sequence on a stream (0 if p is invalid).  For the score pass it holds
- * B H (T-1)(T-2)/2 fp32 candidate scores. */
+/* Stage 5 with the selection inside the attention kernel (the block
+ * selection fused into attention that the Limitations of Section 4 list as
+ * engineering work left open): the same output as ugbs_attend
+ * on the kv_idx of ugbs_route, without materialising kv_idx.  For every
+ * unit (b, h, t) the attended blocks are the forced ones, [0] or [0, t],
+ * and the R best candidates of C(t) by (score descending, lower block
+ * first, -0 == +0), R = (trigger[b, t] ? 2k : k) - |F|, or all of C(t) when
+ * it has at most R; the attention is then as in ugbs_attend (the blocks are
+ * visited in the same order, so the two entry points agree bit for bit).
+ *   scores   : NULL, or [B, H, T, N_B] fp32 tile scores (entries of C(t)
+ *              are read).  NULL: the packed scores that ugbs_score_select
+ *              (without scores_in / scores_out) left in `workspace`.
+ *   trigger  : NULL, or [B, T] uint8 flags (nonzero = expanded).  NULL: the
+ *              flags ugbs_route left in `workspace`.
+ *   workspace: needed when scores or trigger is NULL: the workspace of the
+ *              ugbs_score_select and ugbs_route calls of the same problem,
+ *              issued before this one on the stream.
+ *   Q, K, V, O as for ugbs_attend. */
+UGBS_API int ugbs_attend_select(const ugbs_problem* p, const void* Q, const void* K, const void* V,
+                                const float* scores, const uint8_t* trigger,
+                                const void* workspace, size_t workspace_bytes, void* O,
+                                void* stream);
+
+/* Bytes of device workspace ugbs_score_select (without scores_in/scores_out),
+ * ugbs_route and ugbs_attend_select need for problem p; one workspace
+ * serves the calls of a layer in sequence on a stream (0 if p is invalid).
+ * It holds the route's sections (B T fp32 + B fp32 + B T bytes, each
+ * 256-byte aligned), then B H (T-1)(T-2)/2 fp32 packed candidate scores. */
 UGBS_API size_t ugbs_workspace_bytes(const ugbs_problem* p);
 
 /* Static, human-readable text for a ugbs_status value. */

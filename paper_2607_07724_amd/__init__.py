@@ -20,6 +20,7 @@ __all__ = [
     "KMEAN", "QUEST", "BLOCK", "Problem", "UGBSError", "lib", "library_path",
     "ugbs_block_meta", "ugbs_score_select", "ugbs_route", "ugbs_attend",
     "ugbs_workspace_bytes", "ugbs_status_string", "ugbs_abi_version",
+    "ugbs_attend_select", "prefill_fused",
     "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads", "BAI_TILE_FIELDS", "BAI_HEAD_FIELDS",
     "bai_tile_records", "bai_head_records",
 ]
@@ -106,11 +107,12 @@ def lib():
         L.ugbs_status_string.argtypes = [ctypes.c_int]
         L.ugbs_status_string.restype = ctypes.c_char_p
         L.ugbs_abi_version.argtypes = []
+        L.ugbs_attend_select.argtypes = [pp, P, P, P, P, P, P, ctypes.c_size_t, P, P]
         L.ugbs_noise_scale.argtypes = [pp, P, P, P, P, P]
         L.ugbs_bai_tiles.argtypes = [pp, P, P, P, ctypes.c_int32, P, P]
         L.ugbs_bai_heads.argtypes = [pp, P, P, ctypes.c_int32, P, P]
         for f in ("ugbs_block_meta", "ugbs_score_select", "ugbs_route", "ugbs_attend", "ugbs_abi_version",
-                  "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads"):
+                  "ugbs_attend_select", "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -179,9 +181,9 @@ def ugbs_block_meta(p: Problem, K, meta, stream=None):
 
 def ugbs_score_select(p: Problem, Q, meta, idx_sorted, sigma, scores_in=None, scores_out=None,
                       stream=None, workspace=None):
-    """Stages 2-3 (A.2-A.6): -> idx_sorted [B,H,T,2k] int32, sigma [B,H,T] fp32.
-    Without scores_in/scores_out the tile scores pass through `workspace`
-    (>= ugbs_workspace_bytes(p) bytes)."""
+    """Stages 2-3 (A.2-A.6): -> idx_sorted [B,H,T,2k] int32 (or None: sigma
+    only), sigma [B,H,T] fp32.  Without scores_in/scores_out the tile scores
+    pass through `workspace` (>= ugbs_workspace_bytes(p) bytes)."""
     import torch
     bf = _bf16()
     dev = Q.device
@@ -189,7 +191,7 @@ def ugbs_score_select(p: Problem, Q, meta, idx_sorted, sigma, scores_in=None, sc
     m = _check("meta", meta, (p.batch, p.n_kv_heads, p.NB, p.meta_width, p.head_dim), bf, dev)
     si = _opt("scores_in", scores_in, (p.batch, p.n_heads, p.T, p.NB), (torch.float32,), dev)
     so = _opt("scores_out", scores_out, (p.batch, p.n_heads, p.T, p.NB), (torch.float32,), dev)
-    ix = _check("idx_sorted", idx_sorted, (p.batch, p.n_heads, p.T, p.W), (torch.int32,), dev)
+    ix = _opt("idx_sorted", idx_sorted, (p.batch, p.n_heads, p.T, p.W), (torch.int32,), dev)
     sg = _check("sigma", sigma, (p.batch, p.n_heads, p.T), (torch.float32,), dev)
     ws, nbytes = None, 0
     if workspace is not None:
@@ -201,12 +203,15 @@ def ugbs_score_select(p: Problem, Q, meta, idx_sorted, sigma, scores_in=None, sc
 
 def ugbs_route(p: Problem, sigma, idx_sorted, kv_idx, workspace, sigma_bar=None, tau=None,
                trigger=None, stream=None):
-    """Stage 4 (A.7-A.9): sigma, idx_sorted -> kv_idx (may be idx_sorted itself)."""
+    """Stage 4 (A.7-A.9): sigma, idx_sorted -> kv_idx (may be idx_sorted itself);
+    idx_sorted and kv_idx both None: statistics and trigger flags only."""
     import torch
     dev = sigma.device
     sg = _check("sigma", sigma, (p.batch, p.n_heads, p.T), (torch.float32,))
-    ix = _check("idx_sorted", idx_sorted, (p.batch, p.n_heads, p.T, p.W), (torch.int32,), dev)
-    kv = _check("kv_idx", kv_idx, (p.batch, p.n_heads, p.T, p.W), (torch.int32,), dev)
+    if (idx_sorted is None) != (kv_idx is None):
+        raise ValueError("idx_sorted and kv_idx are given together or not at all")
+    ix = _opt("idx_sorted", idx_sorted, (p.batch, p.n_heads, p.T, p.W), (torch.int32,), dev)
+    kv = _opt("kv_idx", kv_idx, (p.batch, p.n_heads, p.T, p.W), (torch.int32,), dev)
     need = ugbs_workspace_bytes(p)
     if workspace is None or workspace.numel() * workspace.element_size() < need:
         raise ValueError(f"workspace must hold >= {need} bytes")
@@ -233,6 +238,29 @@ def ugbs_attend(p: Problem, Q, K, V, kv_idx, O, stream=None):
     kv = _check("kv_idx", kv_idx, (p.batch, p.n_heads, p.T, width), (torch.int32,), dev)
     o = _check("O", O, (p.batch, p.n_heads, p.seq_len, p.head_dim), bf, dev)
     _raise("ugbs_attend", lib().ugbs_attend(ctypes.byref(p), q, k, v, kv, width, o, _stream(stream)))
+
+
+def ugbs_attend_select(p: Problem, Q, K, V, O, workspace=None, scores=None, trigger=None,
+                       stream=None):
+    """Stage 5 with the selection in the attention kernel: the blocks of
+    ugbs_route's kv_idx, chosen from the tile scores (`scores` [B,H,T,N_B]
+    fp32, or the packed rows ugbs_score_select left in `workspace`) and the
+    trigger flags (`trigger` [B,T] uint8, or ugbs_route's in `workspace`)."""
+    import torch
+    bf = _bf16()
+    dev = Q.device
+    q = _check("Q", Q, (p.batch, p.n_heads, p.seq_len, p.head_dim), bf)
+    k = _check("K", K, (p.batch, p.n_kv_heads, p.seq_len, p.head_dim), bf, dev)
+    v = _check("V", V, (p.batch, p.n_kv_heads, p.seq_len, p.head_dim), bf, dev)
+    o = _check("O", O, (p.batch, p.n_heads, p.seq_len, p.head_dim), bf, dev)
+    sc = _opt("scores", scores, (p.batch, p.n_heads, p.T, p.NB), (torch.float32,), dev)
+    tr = _opt("trigger", trigger, (p.batch, p.T), (torch.uint8,), dev)
+    ws, nbytes = None, 0
+    if workspace is not None:
+        ws = _check("workspace", workspace, tuple(workspace.shape), (workspace.dtype,), dev)
+        nbytes = workspace.numel() * workspace.element_size()
+    _raise("ugbs_attend_select", lib().ugbs_attend_select(ctypes.byref(p), q, k, v, sc, tr, ws, nbytes, o,
+                                                          _stream(stream)))
 
 
 # ---------------------------------------------------------------- diagnostics
@@ -338,6 +366,16 @@ def prefill(p: Problem, Q, K, V, O, bufs: Buffers, stream=None, scores_in=None, 
     ugbs_route(p, bufs.sigma, bufs.idx_sorted, bufs.kv_idx, bufs.workspace, bufs.sigma_bar,
                bufs.tau, bufs.trigger, stream)
     ugbs_attend(p, Q, K, V, bufs.kv_idx, O, stream)
+    return O
+
+
+def prefill_fused(p: Problem, Q, K, V, O, bufs: Buffers, stream=None):
+    """The layer with the selection inside the attention kernel: meta,
+    scores + sigma (no lists), route flags, attention."""
+    ugbs_block_meta(p, K, bufs.meta, stream)
+    ugbs_score_select(p, Q, bufs.meta, None, bufs.sigma, stream=stream, workspace=bufs.workspace)
+    ugbs_route(p, bufs.sigma, None, None, bufs.workspace, bufs.sigma_bar, bufs.tau, bufs.trigger, stream)
+    ugbs_attend_select(p, Q, K, V, O, workspace=bufs.workspace, stream=stream)
     return O
 
 

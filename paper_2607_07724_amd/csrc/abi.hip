@@ -101,7 +101,7 @@ int ugbs_score_select(const ugbs_problem* p, const void* Q, const void* meta,
   Shape s;
   int st = make_shape(p, &s);
   if (st) return st;
-  if (!Q || !meta || !idx_sorted || !sigma) return UGBS_ERR_NULL;
+  if (!Q || !meta || !sigma) return UGBS_ERR_NULL;
   const bool needs_ws = !scores_in && !scores_out;
   if (needs_ws && (!workspace || workspace_bytes < ugbs::ws_total(s))) return UGBS_ERR_WORKSPACE;
   if (!aligned(Q, 16) || !aligned(meta, 16) || !aligned(idx_sorted, 4) || !aligned(sigma, 4) ||
@@ -119,7 +119,7 @@ int ugbs_route(const ugbs_problem* p, const float* sigma, const int32_t* idx_sor
   Shape s;
   int st = make_shape(p, &s);
   if (st) return st;
-  if (!sigma || !idx_sorted || !kv_idx) return UGBS_ERR_NULL;
+  if (!sigma || (!idx_sorted != !kv_idx)) return UGBS_ERR_NULL;
   if (!workspace || workspace_bytes < ugbs::ws_total(s)) return UGBS_ERR_WORKSPACE;
   if (!aligned(sigma, 4) || !aligned(idx_sorted, 4) || !aligned(kv_idx, 4) ||
       !aligned(sigma_bar, 4) || !aligned(tau, 4) || !aligned(workspace, 256))
@@ -129,6 +129,24 @@ int ugbs_route(const ugbs_problem* p, const float* sigma, const int32_t* idx_sor
   return hip_status(ugbs::launch_route(s, n_pop, n_trig, sigma, idx_sorted, kv_idx, sigma_bar,
                                        tau, trigger, workspace,
                                        static_cast<hipStream_t>(stream)));
+}
+
+int ugbs_attend_select(const ugbs_problem* p, const void* Q, const void* K, const void* V,
+                       const float* scores, const uint8_t* trigger, const void* workspace,
+                       size_t workspace_bytes, void* O, void* stream) {
+  Shape s;
+  int st = make_shape(p, &s);
+  if (st) return st;
+  if (!Q || !K || !V || !O) return UGBS_ERR_NULL;
+  const bool needs_ws = !scores || !trigger;
+  if (needs_ws && (!workspace || workspace_bytes < ugbs::ws_total(s))) return UGBS_ERR_WORKSPACE;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) ||
+      !aligned(scores, 4) || (needs_ws && !aligned(workspace, 256)))
+    return UGBS_ERR_ALIGN;
+  return hip_status(ugbs::launch_attend_select(
+      s, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
+      static_cast<const uint16_t*>(V), scores, trigger, needs_ws ? workspace : nullptr,
+      static_cast<uint16_t*>(O), static_cast<hipStream_t>(stream)));
 }
 
 int ugbs_noise_scale(const ugbs_problem* p, const void* Q, const void* meta, double* rough,

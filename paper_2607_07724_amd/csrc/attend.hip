@@ -35,7 +35,7 @@
 #include <atomic>
 #include <type_traits>
 
-#include "ugbs_internal.h"
+#include "select_common.h"
 
 namespace ugbs {
 namespace {
@@ -55,9 +55,11 @@ struct AttnParams {
   int n_units;
   int conc;          // units resident at once on one XCD (rotation period)
   float scale_log2;
+  // in-kernel selection (ugbs_attend_select)
+  const float* sel_scores;    // [B, H, T, N_B] tile scores, or nullptr: packed rows
+  const float* sel_packed;    // packed candidate rows (workspace)
+  const uint8_t* sel_trigger; // [B, T] trigger flags
 };
-
-__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -162,7 +164,7 @@ struct FetchPlan {
   }
 };
 
-template <int D>
+template <int D, bool SEL>
 __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) attend_kernel(AttnParams P) {
   using L = Tile<D>;
   constexpr int KS = D / 32;      // k-steps of QK^T
@@ -198,15 +200,106 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int j_xcd = blockIdx.x >> 3;
   const int start_blk = (int)(((long long)(j_xcd % P.conc) * u.t) / P.conc);
   if (w == 0) {
-    const int32_t* kr = P.kv_idx + rowid * P.kv_width;
     const int nwords = (u.t >> 5) + 1;                 // bitmap words covering blocks 0..t
     for (int i = lane; i < nwords; i += 64) s_bits[i] = 0u;
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_wave_barrier();
-    for (int base = 0; base < P.kv_width; base += 64) {
-      const int sl = base + lane;
-      const int blk = (sl < P.kv_width) ? kr[sl] : -1;
-      if (blk >= 0 && blk <= u.t) atomicOr(&s_bits[blk >> 5], 1u << (blk & 31));
+    if constexpr (!SEL) {
+      const int32_t* kr = P.kv_idx + rowid * P.kv_width;
+      for (int base = 0; base < P.kv_width; base += 64) {
+        const int sl = base + lane;
+        const int blk = (sl < P.kv_width) ? kr[sl] : -1;
+        if (blk >= 0 && blk <= u.t) atomicOr(&s_bits[blk >> 5], 1u << (blk & 31));
+      }
+    } else {
+      // selection (A.4-A.5, A.9) from the tile scores: the forced sink and
+      // self blocks, then the R best candidates of C(t) = {1..t-1} by (score
+      // descending, block ascending), R = (trigger ? rho k : k) - |F|, all
+      // of them when fewer: the same set as the kept prefix of kv_idx
+      const int t = u.t;
+      const int nf = (t == 0) ? 1 : 2;
+      const int nc = (t >= 1) ? t - 1 : 0;
+      // The flag is loaded unconditionally (every (b, t) has one) and moved
+      // to a scalar register: written as a load guarded by nc > 0, the
+      // branch around the load and the k / rho k phi after it came out of
+      // this compiler with the phi's rho k copy executed unconditionally.
+      // With nc == 0, R is 0 whatever the flag.
+      const int flag = __builtin_amdgcn_readfirstlane((int)P.sel_trigger[(size_t)u.b * s.T + t]);
+      const int R = min((flag != 0 ? s.W : s.k) - nf, nc);
+      if (lane == 0) {
+        atomicOr(&s_bits[0], 1u);
+        if (t > 0) atomicOr(&s_bits[t >> 5], 1u << (t & 31));
+      }
+      if (R >= nc) {
+        for (int blk = 1 + lane; blk <= nc; blk += 64) atomicOr(&s_bits[blk >> 5], 1u << (blk & 31));
+      } else {
+        const float* src = P.sel_scores ? P.sel_scores + rowid * s.NB + 1
+                                        : P.sel_packed + packed_row(u.b * s.H + u.h, t, s.T);
+        constexpr int kSlots = UGBS_MAX_BLOCKS / 64;
+        const int nslots = (nc + 63) / 64;
+        uint32_t keys[kSlots];
+#pragma unroll
+        for (int sl = 0; sl < kSlots; ++sl) {
+          const int p = 64 * sl + lane;
+          keys[sl] = (sl < nslots && p < nc) ? order_key(src[p]) : 0u;
+        }
+        // Pre-filter as in the selection kernel: the R-th largest of the
+        // lanes' three largest keys bounds the R-th largest key from below;
+        // the survivors (keys at or above it, in position order) go through
+        // the exact threshold on 4 slots per lane instead of 32.  The K
+        // tile's LDS holds them (no K block is in flight yet).
+        bool done = false;
+        if (R <= 192) {
+          uint32_t top3[3] = {0u, 0u, 0u};
+#pragma unroll
+          for (int sl = 0; sl < kSlots; ++sl) {
+            if (sl < nslots) {
+              const uint32_t x = keys[sl];
+              top3[2] = max(top3[2], min(top3[1], x));
+              top3[1] = max(top3[1], min(top3[0], x));
+              top3[0] = max(top3[0], x);
+            }
+          }
+          bool exact0;
+          const uint32_t t0 = kth_largest<3>(top3, 3, R, &exact0);
+          constexpr int kSurv = 256;
+          uint64_t* s_surv = reinterpret_cast<uint64_t*>(s_k);
+          const uint64_t ltm = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+          int ns = 0;
+#pragma unroll
+          for (int sl = 0; sl < kSlots; ++sl) {
+            if (sl < nslots) {
+              const bool tk = t0 > 0u && keys[sl] >= t0;
+              const uint64_t mk = __ballot(tk);
+              const int at = ns + __popcll(mk & ltm);
+              if (tk && at < kSurv) s_surv[at] = ((uint64_t)keys[sl] << 32) | (uint32_t)(64 * sl + lane);
+              ns += __popcll(mk);
+            }
+          }
+          if (t0 > 0u && ns <= kSurv) {
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            __builtin_amdgcn_wave_barrier();
+            uint32_t k2[kSurv / 64], p2[kSurv / 64];
+#pragma unroll
+            for (int sl = 0; sl < kSurv / 64; ++sl) {
+              const int i = 64 * sl + lane;
+              const uint64_t v = (i < ns) ? s_surv[i] : 0ull;
+              k2[sl] = (uint32_t)(v >> 32);
+              p2[sl] = (uint32_t)v;
+            }
+            select_top_each<kSurv / 64>(k2, (ns + 63) / 64, R, lane, [&](int sl) {
+              const int blk = 1 + (int)p2[sl];
+              atomicOr(&s_bits[blk >> 5], 1u << (blk & 31));
+            });
+            done = true;
+          }
+        }
+        if (!done)
+          select_top_each<kSlots>(keys, nslots, R, lane, [&](int sl) {
+            const int blk = 1 + 64 * sl + lane;
+            atomicOr(&s_bits[blk >> 5], 1u << (blk & 31));
+          });
+      }
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_wave_barrier();
@@ -461,12 +554,12 @@ __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))
   }
 }
 
-// Workgroups of attend_kernel<D> resident at once on one XCD, for the given
+// Workgroups of attend_kernel<D, SEL> resident at once on one XCD, for the given
 // dynamic LDS size (occupancy per CU x CUs per XCD).  Cached per device as
 // one packed word (smem << 32 | value); a stale or missing entry only costs
 // a recomputation.  The value steers the visiting order, never the result.
 constexpr int kMaxDevices = 64;
-template <int D>
+template <int D, bool SEL>
 int xcd_concurrency(size_t smem) {
   static std::atomic<uint64_t> cache[kMaxDevices];
   int dev = -1;
@@ -476,19 +569,20 @@ int xcd_concurrency(size_t smem) {
     if (e != 0 && (e >> 32) == (uint64_t)smem) return (int)(uint32_t)e;
   }
   int per_cu = 0, n_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attend_kernel<D>, 128, smem) != hipSuccess) per_cu = 1;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attend_kernel<D, SEL>, 128, smem) != hipSuccess)
+    per_cu = 1;
   if (dev < 0 || hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) n_cu = 8;
   const int conc = per_cu * n_cu / 8 > 0 ? per_cu * n_cu / 8 : 1;
   if (dev >= 0) cache[dev].store(((uint64_t)smem << 32) | (uint32_t)conc, std::memory_order_relaxed);
   return conc;
 }
 
-template <int D>
+template <int D, bool SEL>
 hipError_t launch_t(AttnParams P, hipStream_t stream) {
   const size_t smem = sizeof(int32_t) * (size_t)P.kv_width;
   const int grid = ((P.n_units + 7) / 8) * 8;
-  P.conc = xcd_concurrency<D>(smem);
-  attend_kernel<D><<<grid, 128, smem, stream>>>(P);
+  P.conc = xcd_concurrency<D, SEL>(smem);
+  attend_kernel<D, SEL><<<grid, 128, smem, stream>>>(P);
   return hipGetLastError();
 }
 
@@ -497,7 +591,7 @@ hipError_t launch_t(AttnParams P, hipStream_t stream) {
 hipError_t launch_attend(const Shape& s, const uint16_t* Q, const uint16_t* K,
                          const uint16_t* V, const int32_t* kv_idx, int kv_width,
                          uint16_t* O, hipStream_t stream) {
-  AttnParams P;
+  AttnParams P{};
   P.s = s;
   P.Q = Q;
   P.K = K;
@@ -507,7 +601,27 @@ hipError_t launch_attend(const Shape& s, const uint16_t* Q, const uint16_t* K,
   P.kv_width = kv_width;
   P.n_units = s.B * s.H * s.T;
   P.scale_log2 = s.scale * 1.4426950408889634f;
-  return s.d == 128 ? launch_t<128>(P, stream) : launch_t<64>(P, stream);
+  return s.d == 128 ? launch_t<128, false>(P, stream) : launch_t<64, false>(P, stream);
+}
+
+hipError_t launch_attend_select(const Shape& s, const uint16_t* Q, const uint16_t* K,
+                                const uint16_t* V, const float* scores, const uint8_t* trigger,
+                                const void* workspace, uint16_t* O, hipStream_t stream) {
+  AttnParams P{};
+  P.s = s;
+  P.Q = Q;
+  P.K = K;
+  P.V = V;
+  P.O = O;
+  // at most |F| + (rho k - |F|) distinct blocks per tile, and never more than t + 1
+  P.kv_width = s.W < s.NB ? s.W : s.NB;
+  P.n_units = s.B * s.H * s.T;
+  P.scale_log2 = s.scale * 1.4426950408889634f;
+  const unsigned char* ws = static_cast<const unsigned char*>(workspace);
+  P.sel_scores = scores;
+  P.sel_packed = ws ? reinterpret_cast<const float*>(ws + ws_scores_off(s)) : nullptr;
+  P.sel_trigger = trigger ? trigger : ws + ws_trigger_off(s);
+  return s.d == 128 ? launch_t<128, true>(P, stream) : launch_t<64, true>(P, stream);
 }
 
 }  // namespace ugbs

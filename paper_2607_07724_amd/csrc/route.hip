@@ -139,7 +139,7 @@ hipError_t launch_route(const Shape& s, int n_pop, int n_trig, const float* sigm
   P.ws_trigger = ws + ws_trigger_off(s);
   route_stats_kernel<<<s.B, kStatsThreads, 0, stream>>>(P);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || !kv_idx) return e;  // no lists to patch: flags only
   const long n_slots = (long)s.B * s.H * s.T * s.W;
   long blocks = (n_slots + 255) / 256;
   if (blocks > 65536) blocks = 65536;

@@ -62,14 +62,6 @@ struct SelParams {
   int row_lds;    // bytes of per-wave LDS of the score kernel (one row of scores)
 };
 
-// Offset (floats) of the packed candidate row of unit (bh, t): rows of one
-// (b, h) follow each other, row t holding t-1 scores.
-__device__ __forceinline__ size_t packed_row(int bh, int t, int T) {
-  const size_t tri = (T >= 2) ? (size_t)(T - 1) * (T - 2) / 2 : 0;
-  const size_t off = (t >= 2) ? (size_t)(t - 1) * (t - 2) / 2 : 0;
-  return (size_t)bh * tri + off;
-}
-
 // max over the four 16-lane rows (lanes l, l^16, l^32, l^48) with the gfx950
 // row-swap permutes: permlane32_swap pairs row r with r^2, permlane16_swap
 // row r with r^1 (VALU only, no LDS round trip).
@@ -355,13 +347,15 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
   const int nc = (t >= 1) ? t - 1 : 0;
   const int m = s.k - nf;
   const int W = s.W;
-  const int R = min(W - nf, nc);
+  // without idx_sorted only sigma is wanted: the m + 1 largest suffice
+  const int R = P.idx_sorted ? min(W - nf, nc) : min(m + 1, nc);
   uint64_t* s_sel = reinterpret_cast<uint64_t*>(smem + w * P.wave_lds);
   const float* src = PACKED ? P.scratch + packed_row(b * s.H + h, t, s.T) : P.scores_in + row * s.NB + 1;
 
-  int32_t* out = P.idx_sorted + row * W;
+  int32_t* out = P.idx_sorted ? P.idx_sorted + row * W : nullptr;
   if (nc == 0) {
-    for (int p = lane; p < W; p += 64) out[p] = (p < nf) ? (p == 0 ? 0 : t) : s.NB;
+    if (out)
+      for (int p = lane; p < W; p += 64) out[p] = (p < nf) ? (p == 0 ? 0 : t) : s.NB;
     if (lane == 0) P.sigma[row] = -1.0f;
     return;
   }
@@ -489,7 +483,7 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
   }
 
   // ---- outputs --------------------------------------------------------------
-  for (int p = lane; p < W; p += 64) {
+  for (int p = lane; out && p < W; p += 64) {
     int v;
     if (p < nf)
       v = (p == 0) ? 0 : t;
@@ -582,7 +576,8 @@ hipError_t launch_score_select(const Shape& s, const uint16_t* Q, const uint16_t
   P.scores_out = scores_out;
   P.idx_sorted = idx_sorted;
   P.sigma = sigma;
-  P.scratch = static_cast<float*>(workspace);
+  P.scratch = workspace ? reinterpret_cast<float*>(static_cast<unsigned char*>(workspace) + ws_scores_off(s))
+                        : nullptr;
   int cap = 2;
   const int rmax = s.W < s.NB ? s.W : s.NB;
   while (cap < rmax) cap <<= 1;

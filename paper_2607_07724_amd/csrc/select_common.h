@@ -105,6 +105,38 @@ __device__ __forceinline__ void select_top(const uint32_t (&key)[S], const uint3
   }
 }
 
+// The same R largest keys as select_top, reported through
+// take(slot) on the lane that holds each of them (no order, no storage).
+// Returns nothing; every lane of the wave must call it.
+template <int S, typename Take>
+__device__ __forceinline__ void select_top_each(const uint32_t (&key)[S], int nslots, int R, int lane,
+                                                Take&& take) {
+  bool exact;
+  const uint32_t thr = kth_largest<S>(key, nslots, R, &exact);
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  int above = 0;
+#pragma unroll
+  for (int sl = 0; sl < S; ++sl) {
+    if (sl < nslots) {
+      const bool tk = exact ? (key[sl] >= thr) : (key[sl] > thr);
+      if (tk) take(sl);
+      above += __popcll(__ballot(tk));
+    }
+  }
+  if (!exact) {
+    int need = R - above;
+#pragma unroll
+    for (int sl = 0; sl < S; ++sl) {
+      if (sl < nslots && need > 0) {
+        const bool eq = key[sl] == thr;
+        const uint64_t mk = __ballot(eq);
+        if (eq && __popcll(mk & lt_mask) < need) take(sl);
+        need -= min(__popcll(mk), need);
+      }
+    }
+  }
+}
+
 // LDS hand-off between lanes of one wave: LDS operations of a wave complete
 // in order, so waiting for this wave's outstanding ones is enough.
 __device__ __forceinline__ void wave_lds_sync() {

@@ -46,6 +46,12 @@ hipError_t launch_bai_heads(const Shape& s, const ugbs_bai_tile* tiles, const fl
 hipError_t launch_attend(const Shape& s, const uint16_t* Q, const uint16_t* K,
                          const uint16_t* V, const int32_t* kv_idx, int kv_width,
                          uint16_t* O, hipStream_t stream);
+// Attention with the selection done in the kernel: scores (full layout) or
+// the packed rows in `workspace`; trigger flags or the ones ugbs_route left
+// in `workspace`.
+hipError_t launch_attend_select(const Shape& s, const uint16_t* Q, const uint16_t* K,
+                                const uint16_t* V, const float* scores, const uint8_t* trigger,
+                                const void* workspace, uint16_t* O, hipStream_t stream);
 
 // Route workspace layout: sigma_bar [B*T] f32 | tau [B] f32 | trigger [B*T] u8.
 inline size_t ws_align(size_t x) { return (x + 255) & ~size_t(255); }
@@ -55,11 +61,19 @@ inline size_t ws_trigger_off(const Shape& s) {
   return ws_tau_off(s) + ws_align(sizeof(float) * size_t(s.B));
 }
 inline size_t ws_route_total(const Shape& s) { return ws_trigger_off(s) + ws_align(size_t(s.B) * s.T); }
-// One workspace serves both calls: the packed scores are dead once
-// ugbs_score_select returns, and ugbs_route only needs its own sections.
-inline size_t ws_total(const Shape& s) {
-  const size_t a = ws_route_total(s), b = ws_align(score_scratch_bytes(s));
-  return a > b ? a : b;
+// One workspace serves the whole layer: the route sections first, then the
+// packed candidate scores of the score kernel (which ugbs_attend_select may
+// read after ugbs_route has written the trigger flags).
+inline size_t ws_scores_off(const Shape& s) { return ws_route_total(s); }
+inline size_t ws_total(const Shape& s) { return ws_scores_off(s) + ws_align(score_scratch_bytes(s)); }
+
+// Offset (floats) of the packed candidate row of unit (bh, t) in the packed
+// score section: rows of one (b, h) follow each other, row t holding the
+// t - 1 scores of blocks 1..t-1.
+__host__ __device__ inline size_t packed_row(int bh, int t, int T) {
+  const size_t tri = (T >= 2) ? (size_t)(T - 1) * (T - 2) / 2 : 0;
+  const size_t off = (t >= 2) ? (size_t)(t - 1) * (t - 2) / 2 : 0;
+  return (size_t)bh * tri + off;
 }
 
 // Work-unit ordering used by the per-(tile, head) kernels: consecutive

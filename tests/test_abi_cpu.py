@@ -90,6 +90,7 @@ def test_invalid_problem_rejected_by_every_entry_point(kw, code):
     assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, fake, fake, fake, 1 << 30, None) == want
     assert L.ugbs_route(ctypes.byref(p), fake, fake, fake, None, None, None, fake, 1 << 20, None) == want
     assert L.ugbs_attend(ctypes.byref(p), fake, fake, fake, fake, 8, fake, None) == want
+    assert L.ugbs_attend_select(ctypes.byref(p), fake, fake, fake, None, None, fake, 1 << 30, fake, None) == want
     assert L.ugbs_workspace_bytes(ctypes.byref(p)) == 0
     assert L.ugbs_noise_scale(ctypes.byref(p), fake, fake, fake, fake, None) == want
     assert L.ugbs_bai_tiles(ctypes.byref(p), fake, fake, fake, 4, fake, None) == want
@@ -104,11 +105,16 @@ def test_null_problem_and_null_pointers():
     p = good()
     assert L.ugbs_block_meta(ctypes.byref(p), None, fake, None) == ERR_NULL
     assert L.ugbs_block_meta(ctypes.byref(p), fake, None, None) == ERR_NULL
-    assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, None, fake, fake, 1 << 30, None) == ERR_NULL
     assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, fake, None, fake, 1 << 30, None) == ERR_NULL
     assert L.ugbs_score_select(ctypes.byref(p), None, fake, None, None, fake, fake, fake, 1 << 30, None) == ERR_NULL
     assert L.ugbs_route(ctypes.byref(p), None, fake, fake, None, None, None, fake, 1 << 20, None) == ERR_NULL
     assert L.ugbs_route(ctypes.byref(p), fake, fake, None, None, None, None, fake, 1 << 20, None) == ERR_NULL
+    assert L.ugbs_route(ctypes.byref(p), fake, None, fake, None, None, None, fake, 1 << 20, None) == ERR_NULL
+    for i in range(4):
+        args = [fake] * 4
+        args[i] = None
+        assert L.ugbs_attend_select(ctypes.byref(p), args[0], args[1], args[2], fake, fake, None, 0,
+                                    args[3], None) == ERR_NULL
     for i in range(5):
         args = [fake] * 5
         args[i] = None
@@ -147,16 +153,33 @@ def test_workspace_bytes_grows_with_tiles():
 
 
 @pytest.mark.parametrize("B,H,N", [(1, 4, 1024), (2, 32, 131072), (1, 28, 65536), (1, 2, 64), (1, 2, 128)])
-def test_workspace_holds_the_packed_candidate_scores(B, H, N):
-    """B H (T-1)(T-2)/2 fp32 candidate scores (rows t = 2..T-1 hold t-1 each),
-    and the route sections, whichever is larger, rounded up to 256 bytes."""
+def test_workspace_holds_route_sections_then_packed_scores(B, H, N):
+    """The route's sections (B T fp32 | B fp32 | B T bytes, each rounded up
+    to 256 bytes), then B H (T-1)(T-2)/2 fp32 candidate scores (rows t =
+    2..T-1 hold t-1 each), rounded up to 256 bytes."""
     T = N // 64
+    up = lambda x: (x + 255) // 256 * 256
     packed = 4 * B * H * sum(max(t - 1, 0) for t in range(T))
-    route = 4 * B * T + 4 * B + B * T
+    route = up(4 * B * T) + up(4 * B) + up(B * T)
     got = ugbs.ugbs_workspace_bytes(ugbs.Problem.make(B, H, 1, N, 64, 3, 0.25))
-    assert got % 256 == 0
-    assert got >= max(packed, route)
-    assert got < max(packed, route) + 3 * 256
+    assert got == route + up(packed)
+
+
+def test_attend_select_checks():
+    L = ugbs.lib()
+    p = good()
+    fake = ctypes.c_void_p(0x100000)
+    need = L.ugbs_workspace_bytes(ctypes.byref(p))
+    ERR_WS, ERR_ALIGN = _enum("UGBS_ERR_WORKSPACE"), _enum("UGBS_ERR_ALIGN")
+    # without scores or without trigger the workspace is read
+    assert L.ugbs_attend_select(ctypes.byref(p), fake, fake, fake, None, fake, None, 0, fake, None) == ERR_WS
+    assert L.ugbs_attend_select(ctypes.byref(p), fake, fake, fake, fake, None, fake, need - 1, fake, None) == ERR_WS
+    assert L.ugbs_attend_select(ctypes.byref(p), fake, fake, fake, None, None, ctypes.c_void_p(0x100010),
+                                need, fake, None) == ERR_ALIGN
+    assert L.ugbs_attend_select(ctypes.byref(p), fake, ctypes.c_void_p(0x100008), fake, fake, fake, None, 0,
+                                fake, None) == ERR_ALIGN
+    assert L.ugbs_attend_select(ctypes.byref(p), fake, fake, fake, ctypes.c_void_p(0x100002), fake, None, 0,
+                                fake, None) == ERR_ALIGN
 
 
 def test_binding_rejects_host_tensors_before_calling():
