@@ -31,8 +31,8 @@ def lib():
         i32, i64, f64 = ctypes.c_int, ctypes.c_long, ctypes.c_double
         L.orc_block_meta.argtypes = [i32, i32, i32, i32, i32, P, P, i32]
         L.orc_tile_scores.argtypes = [i32, i32, i32, i32, i32, i32, P, P, i64, P, P, i32]
-        L.orc_select.argtypes = [i32, i32, i64, P, P, P, P]
-        L.orc_route.argtypes = [i32, i32, i32, i32, f64, P, P, P, P, P, P]
+        L.orc_select.argtypes = [i32, i32, i32, i64, P, P, P, P]
+        L.orc_route.argtypes = [i32, i32, i32, i32, i32, f64, P, P, P, P, P, P]
         L.orc_attend.argtypes = [i32, i32, i32, i32, f64, P, P, P, P, i32, i32, i64, P, P, i32]
         L.orc_row_roughness.argtypes = [i32, i32, i32, i32, i32, P, P, i64, P, P, i32]
         L.orc_row_roughness.restype = ctypes.c_int
@@ -101,8 +101,8 @@ def tile_scores(backbone, Q, meta, Hkv, units=None, nthreads=None):
     return out.reshape(B, H, NB, NB) if full else out
 
 
-def select(tile_score, k, t_of_row=None):
-    """A.4-A.6: tile_score [..., N_B] fp32 -> idx_sorted [..., 2k] int32, sigma [...] fp32.
+def select(tile_score, k, t_of_row=None, rho=2):
+    """A.4-A.6: tile_score [..., N_B] fp32 -> idx_sorted [..., rho k] int32, sigma [...] fp32.
 
     If ``t_of_row`` is None the second-to-last axis of a [B,H,T,N_B] array is t."""
     ts = _c(tile_score, np.float32)
@@ -113,15 +113,17 @@ def select(tile_score, k, t_of_row=None):
         t_of_row = np.broadcast_to(np.arange(T, dtype=np.int32), lead)
     t_of_row = _c(np.asarray(t_of_row, np.int32).reshape(-1), np.int32)
     rows = t_of_row.shape[0]
-    idx = np.empty((rows, 2 * k), np.int32)
+    W = rho * k
+    idx = np.empty((rows, W), np.int32)
     sig = np.empty((rows,), np.float32)
-    rc = lib().orc_select(NB, k, rows, _ptr(t_of_row), _ptr(ts.reshape(rows, NB)), _ptr(idx), _ptr(sig))
+    rc = lib().orc_select(NB, k, rho, rows, _ptr(t_of_row), _ptr(ts.reshape(rows, NB)), _ptr(idx),
+                          _ptr(sig))
     assert rc == 0
-    return idx.reshape(*lead, 2 * k), sig.reshape(lead)
+    return idx.reshape(*lead, W), sig.reshape(lead)
 
 
-def route(sigma, idx_sorted, k, q):
-    """A.7-A.9: sigma [B,H,T], idx_sorted [B,H,T,2k] -> kv_idx, sigma_bar [B,T], tau [B], trigger [B,T]."""
+def route(sigma, idx_sorted, k, q, rho=2):
+    """A.7-A.9: sigma [B,H,T], idx_sorted [B,H,T,rho k] -> kv_idx, sigma_bar [B,T], tau [B], trigger [B,T]."""
     sigma = _c(sigma, np.float32)
     idx_sorted = _c(idx_sorted, np.int32)
     B, H, T = sigma.shape
@@ -129,7 +131,8 @@ def route(sigma, idx_sorted, k, q):
     sb = np.empty((B, T), np.float32)
     tau = np.empty((B,), np.float32)
     trig = np.empty((B, T), np.uint8)
-    rc = lib().orc_route(B, H, T, k, float(q), _ptr(sigma), _ptr(idx_sorted), _ptr(kv), _ptr(sb),
+    assert idx_sorted.shape[-1] == rho * k
+    rc = lib().orc_route(B, H, T, k, rho, float(q), _ptr(sigma), _ptr(idx_sorted), _ptr(kv), _ptr(sb),
                          _ptr(tau), _ptr(trig))
     assert rc == 0
     return kv, sb, tau, trig

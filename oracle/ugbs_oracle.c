@@ -253,13 +253,13 @@ static int cand_cmp(const void* pa, const void* pb) {
 }
 
 /* One row: tile t, scores row[0..N_B) (only C(t) = 1..t-1 is read).
- * idx_out gets 2k entries: F(t) = [0] (t = 0) or [0, t], then the candidates
- * by (score desc, block asc), truncated to 2k and padded with N_B.
+ * idx_out gets W = rho k entries: F(t) = [0] (t = 0) or [0, t], then the
+ * candidates by (score desc, block asc), truncated to W and padded with N_B
+ * (Section 3 step 5: the sorted prefix is cut at rho k).
  * sigma_out: (c[m-1] - c[m]) / (c[0] - c[m]) over the sorted candidates with
  * m = k - |F|, fp32; 0 if the denominator is 0; -1 if |C| <= m. */
-static void select_row(int t, int NB, int k, const float* row, int32_t* idx_out,
+static void select_row(int t, int NB, int k, int W, const float* row, int32_t* idx_out,
                        float* sigma_out) {
-  int W = 2 * k;
   int nf = (t == 0) ? 1 : 2;
   int nc = (t >= 1) ? t - 1 : 0;
   int m = k - nf;
@@ -284,12 +284,13 @@ static void select_row(int t, int NB, int k, const float* row, int32_t* idx_out,
   free(c);
 }
 
-int orc_select(int NB, int k, long n_rows, const int32_t* t_of_row,
+int orc_select(int NB, int k, int rho, long n_rows, const int32_t* t_of_row,
                const float* tile_score, int32_t* idx_sorted, float* sigma) {
-  if (k < 3) return -1;
+  if (k < 3 || rho < 1) return -1;
+  int W = rho * k;
   for (long r = 0; r < n_rows; ++r)
-    select_row(t_of_row[r], NB, k, tile_score + (size_t)r * NB,
-               idx_sorted + (size_t)r * 2 * k, sigma + r);
+    select_row(t_of_row[r], NB, k, W, tile_score + (size_t)r * NB,
+               idx_sorted + (size_t)r * W, sigma + r);
   return 0;
 }
 
@@ -308,14 +309,15 @@ static int in_population(int t, int k) {
   return nc > k - nf;
 }
 
-/* sigma [B, H, T], idx_sorted [B, H, T, 2k] -> kv_idx [B, H, T, 2k],
+/* sigma [B, H, T], idx_sorted [B, H, T, W] -> kv_idx [B, H, T, W] with
+ * W = rho k (a triggered tile keeps all W slots, the others the first k),
  * sigma_bar [B, T] (-1 outside the population), tau [B] (-1 when nothing
  * triggers), trigger [B, T]. */
-int orc_route(int B, int H, int T, int k, double q, const float* sigma,
+int orc_route(int B, int H, int T, int k, int rho, double q, const float* sigma,
               const int32_t* idx_sorted, int32_t* kv_idx, float* sigma_bar,
               float* tau, uint8_t* trigger) {
-  if (q < 0.0 || q > 1.0 || k < 3) return -1;
-  int W = 2 * k, NB = T;
+  if (q < 0.0 || q > 1.0 || k < 3 || rho < 1) return -1;
+  int W = rho * k, NB = T;
   float* pop = (float*)malloc(sizeof(float) * (size_t)(T > 0 ? T : 1));
   for (int b = 0; b < B; ++b) {
     int n = 0;

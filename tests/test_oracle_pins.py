@@ -472,3 +472,52 @@ def test_attend_units_subset_equals_full():
     sub = oracle.attend(inp.Q, inp.K, inp.V, kv_idx=kv[0, [1, 0], [3, 2]], units=units)
     np.testing.assert_array_equal(sub[0], full[0, 1, 3 * BLK:4 * BLK])
     np.testing.assert_array_equal(sub[1], full[0, 0, 2 * BLK:3 * BLK])
+
+
+# ---------------------------------------------------------------- expansion factor rho
+
+@pytest.mark.parametrize("rho", [1, 3, 4])
+def test_rho_expansion(rho):
+    """Section 3 step 5 with a general factor: kv_idx rows have rho k slots;
+    a triggered tile keeps all of them, the others the first k.  q = 1 with
+    budget k equals q = 0 with budget rho k on the first rho k slots; rho = 1
+    never expands (kv_idx equals the plain top-k prefix whatever q); the
+    sorted prefix of rho k is the prefix of the rho' k list for rho' > rho
+    (Observation 1); the mean kept count grows by k (rho - 1) q."""
+    w, inp, S = _c1_scores()
+    T = w.T
+    for k in (3, 4):
+        idx, sig = oracle.select(S, k, rho=rho)
+        assert idx.shape[-1] == rho * k
+        idx8, sig8 = oracle.select(S, k, rho=8)
+        assert np.array_equal(idx, idx8[..., :rho * k]) and np.array_equal(sig, sig8)
+        kv1, *_ = oracle.route(sig, idx, k, 1.0, rho=rho)
+        idxw, _ = oracle.select(S, rho * k, rho=1)
+        kvw, *_ = oracle.route(*oracle.select(S, rho * k, rho=1)[::-1], rho * k, 0.0, rho=1)
+        assert np.array_equal(kv1, kvw) and np.array_equal(kvw, idxw)
+        kvq, _, _, trig = oracle.route(sig, idx, k, 0.3, rho=rho)
+        for b in range(w.B):
+            for t in range(T):
+                keep = rho * k if trig[b, t] else k
+                assert np.array_equal(kvq[b, :, t, :keep], idx[b, :, t, :keep])
+                assert np.all(kvq[b, :, t, keep:] == T)
+        if rho == 1:
+            assert np.array_equal(kvq, idx)
+    # mean slots over population tiles with >= rho k visible blocks: k (1 + (rho - 1) n_trig / n)
+    g = np.random.default_rng(9)
+    B, H, T, k = 1, 2, 160, 3
+    P = oracle.population(T, k)
+    V = np.arange(T) + 1
+    sigma = g.random((B, H, T)).astype(np.float32)
+    S2 = np.full((B, H, T, T), -np.inf, np.float32)
+    for t in range(T):
+        S2[0, :, t, 1:t] = g.standard_normal((H, max(t - 1, 0)))
+    idx, _ = oracle.select(S2, k, rho=rho)
+    kv, _, _, trig = oracle.route(sigma, idx, k, 0.25, rho=rho)
+    slots = (kv[0] != T).sum(axis=-1)
+    expect = np.where(trig[0].astype(bool), np.minimum(rho * k, V), np.minimum(k, V))
+    assert np.array_equal(slots, np.broadcast_to(expect, slots.shape))
+    big = P & (V >= rho * k)
+    n, n_trig = int(P.sum()), math.ceil(0.25 * int(P.sum()))
+    extra = int(np.sum((np.minimum(rho * k, V) - rho * k)[P & ~big & trig[0].astype(bool)]))
+    assert slots[:, P].sum(axis=1).tolist() == [k * n + (rho - 1) * k * n_trig + extra] * H
