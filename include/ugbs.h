@@ -62,16 +62,17 @@ extern "C" {
 #define UGBS_API
 #endif
 
-#define UGBS_ABI_VERSION 4
+#define UGBS_ABI_VERSION 5
 #define UGBS_BLOCK 64          /* BLOCK_M = BLOCK_N = 64 tokens (Section 3.1, 3.2) */
 #define UGBS_MAX_BLOCKS 2048   /* N_B <= 2048, i.e. N <= 131072 */
-#define UGBS_MAX_KV_WIDTH 4096 /* kv_width accepted by ugbs_attend; k_budget <= 2048 */
+#define UGBS_MAX_KV_WIDTH 4096 /* kv_width accepted by ugbs_attend; rho * k_budget <= 4096 */
+#define UGBS_MAX_RHO 8         /* expansion factor rho in 1..8 */
 
 typedef enum {
   UGBS_OK = 0,
   UGBS_ERR_NULL = 1,      /* a required pointer is NULL */
   UGBS_ERR_SHAPE = 2,     /* batch/heads/seq_len/head_dim/block/kv_width invalid */
-  UGBS_ERR_BUDGET = 3,    /* k_budget outside [3, UGBS_MAX_KV_WIDTH / 2] */
+  UGBS_ERR_BUDGET = 3,    /* k_budget < 3, rho outside [1, 8], or rho k_budget > 4096 */
   UGBS_ERR_Q = 4,         /* q outside [0, 1] or NaN */
   UGBS_ERR_BACKBONE = 5,  /* backbone not one of ugbs_backbone */
   UGBS_ERR_ALIGN = 6,     /* a pointer is not aligned as documented */
@@ -86,21 +87,22 @@ typedef enum {
 typedef enum { UGBS_KMEAN = 0, UGBS_QUEST = 1 } ugbs_backbone;
 
 /* Problem description, following the paper's problem statement:
- * Q, K, V shapes, block size, k_budget, q and the backbone.  rho is fixed
- * at 2, so every kv_idx row has 2 * k_budget slots. */
+ * Q, K, V shapes, block size, k_budget, q, the backbone and the expansion
+ * factor rho (Section 3 step 5; the paper uses rho = 2).  Every kv_idx row
+ * has W = rho * k_budget slots; "2k" below stands for W. */
 typedef struct ugbs_problem {
   int32_t batch;        /* B >= 1 */
   int32_t n_heads;      /* H >= 1, a multiple of n_kv_heads */
   int32_t n_kv_heads;   /* H_kv >= 1 */
   int32_t seq_len;      /* N: a positive multiple of 64, N / 64 <= UGBS_MAX_BLOCKS */
-  int32_t head_dim;     /* d: 64 or 128 */
+  int32_t head_dim;     /* d: 64, 128 or 256 */
   int32_t block;        /* must be 64 */
-  int32_t k_budget;     /* k: 3 <= k <= UGBS_MAX_KV_WIDTH / 2; counts the forced sink and
+  int32_t k_budget;     /* k >= 3 with rho k <= UGBS_MAX_KV_WIDTH; counts the forced sink and
                            self blocks; with k >= N_B every tile keeps all visible blocks */
   int32_t backbone;     /* ugbs_backbone */
   double q;             /* trigger fraction, 0 <= q <= 1 */
   float softmax_scale;  /* attention logit scale; 0 means 1/sqrt(head_dim) */
-  int32_t reserved;     /* must be 0 */
+  int32_t rho;          /* expansion factor, 1..UGBS_MAX_RHO; 0 means 2 */
 } ugbs_problem;
 
 /* Stage 1 -- block metadata (A.1; Eq. (quest-score) for Quest).

@@ -56,12 +56,12 @@ class Problem(ctypes.Structure):
         ("backbone", ctypes.c_int32),
         ("q", ctypes.c_double),
         ("softmax_scale", ctypes.c_float),
-        ("reserved", ctypes.c_int32),
+        ("rho", ctypes.c_int32),
     ]
 
     @classmethod
-    def make(cls, B, H, Hkv, N, d, k, q, backbone=KMEAN, scale=0.0, block=BLOCK):
-        return cls(B, H, Hkv, N, d, block, k, backbone, float(q), float(scale), 0)
+    def make(cls, B, H, Hkv, N, d, k, q, backbone=KMEAN, scale=0.0, block=BLOCK, rho=2):
+        return cls(B, H, Hkv, N, d, block, k, backbone, float(q), float(scale), rho)
 
     @property
     def NB(self) -> int:
@@ -73,7 +73,7 @@ class Problem(ctypes.Structure):
 
     @property
     def W(self) -> int:
-        return 2 * self.k_budget
+        return (self.rho or 2) * self.k_budget
 
     @property
     def meta_width(self) -> int:

@@ -16,15 +16,17 @@ int make_shape(const ugbs_problem* p, Shape* s) {
   if (!p) return UGBS_ERR_NULL;
   if (p->batch < 1 || p->n_heads < 1 || p->n_kv_heads < 1 || p->n_heads % p->n_kv_heads)
     return UGBS_ERR_SHAPE;
-  if (p->head_dim != 64 && p->head_dim != 128) return UGBS_ERR_SHAPE;
-  if (p->block != UGBS_BLOCK || p->reserved != 0) return UGBS_ERR_SHAPE;
+  if (p->head_dim != 64 && p->head_dim != 128 && p->head_dim != 256) return UGBS_ERR_SHAPE;
+  if (p->block != UGBS_BLOCK) return UGBS_ERR_SHAPE;
   if (p->seq_len < UGBS_BLOCK || p->seq_len % UGBS_BLOCK) return UGBS_ERR_SHAPE;
   const int NB = p->seq_len / UGBS_BLOCK;
   if (NB > UGBS_MAX_BLOCKS) return UGBS_ERR_SHAPE;
   // unit counts index grids with int; element counts use size_t
   if ((int64_t)p->batch * p->n_heads * NB > (int64_t)INT32_MAX / 2) return UGBS_ERR_SHAPE;
   if (p->backbone != UGBS_KMEAN && p->backbone != UGBS_QUEST) return UGBS_ERR_BACKBONE;
-  if (p->k_budget < 3 || p->k_budget > UGBS_MAX_KV_WIDTH / 2) return UGBS_ERR_BUDGET;
+  const int rho = p->rho == 0 ? 2 : p->rho;
+  if (rho < 1 || rho > UGBS_MAX_RHO) return UGBS_ERR_BUDGET;
+  if (p->k_budget < 3 || (int64_t)rho * p->k_budget > UGBS_MAX_KV_WIDTH) return UGBS_ERR_BUDGET;
   if (!(p->q >= 0.0 && p->q <= 1.0)) return UGBS_ERR_Q;
   if (!std::isfinite(p->softmax_scale) || p->softmax_scale < 0.0f) return UGBS_ERR_SCALE;
   s->B = p->batch;
@@ -36,7 +38,8 @@ int make_shape(const ugbs_problem* p, Shape* s) {
   s->NB = NB;
   s->T = NB;
   s->k = p->k_budget;
-  s->W = 2 * p->k_budget;
+  s->W = rho * p->k_budget;
+  s->rho = rho;
   s->backbone = p->backbone;
   s->q = p->q;
   s->scale = p->softmax_scale > 0.0f ? p->softmax_scale : 1.0f / std::sqrt((float)p->head_dim);
@@ -67,7 +70,7 @@ const char* ugbs_status_string(int status) {
     case UGBS_OK: return "ok";
     case UGBS_ERR_NULL: return "a required pointer is NULL";
     case UGBS_ERR_SHAPE: return "invalid shape (batch, heads, seq_len, head_dim, block or kv_width)";
-    case UGBS_ERR_BUDGET: return "k_budget outside [3, UGBS_MAX_KV_WIDTH / 2]";
+    case UGBS_ERR_BUDGET: return "k_budget < 3, rho outside [1, UGBS_MAX_RHO] or rho * k_budget > UGBS_MAX_KV_WIDTH";
     case UGBS_ERR_Q: return "q outside [0, 1]";
     case UGBS_ERR_BACKBONE: return "unknown backbone";
     case UGBS_ERR_ALIGN: return "pointer misaligned";

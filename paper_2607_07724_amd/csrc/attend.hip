@@ -164,8 +164,15 @@ struct FetchPlan {
   }
 };
 
+// d <= 128: two waves per SIMD; d = 256 needs twice the accumulators and
+// query registers (O^T alone is 128 fp32 per lane), so one wave per SIMD
+// with the matrix accumulators in the AGPR half of the register file.
+template <int D>
+constexpr int kWavesPerEU = D > 128 ? 1 : 2;
+
 template <int D, bool SEL>
-__global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) attend_kernel(AttnParams P) {
+__global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(kWavesPerEU<D>, kWavesPerEU<D>)))
+attend_kernel(AttnParams P) {
   using L = Tile<D>;
   constexpr int KS = D / 32;      // k-steps of QK^T
   constexpr int DT = D / 16;      // 16-channel tiles of O^T
@@ -581,6 +588,11 @@ template <int D, bool SEL>
 hipError_t launch_t(AttnParams P, hipStream_t stream) {
   const size_t smem = sizeof(int32_t) * (size_t)P.kv_width;
   const int grid = ((P.n_units + 7) / 8) * 8;
+  if (D > 128) {  // the K and V tiles alone take 64 KB of static LDS
+    const hipError_t e = hipFuncSetAttribute((const void*)attend_kernel<D, SEL>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+  }
   P.conc = xcd_concurrency<D, SEL>(smem);
   attend_kernel<D, SEL><<<grid, 128, smem, stream>>>(P);
   return hipGetLastError();
@@ -601,6 +613,7 @@ hipError_t launch_attend(const Shape& s, const uint16_t* Q, const uint16_t* K,
   P.kv_width = kv_width;
   P.n_units = s.B * s.H * s.T;
   P.scale_log2 = s.scale * 1.4426950408889634f;
+  if (s.d == 256) return launch_t<256, false>(P, stream);
   return s.d == 128 ? launch_t<128, false>(P, stream) : launch_t<64, false>(P, stream);
 }
 
@@ -621,6 +634,7 @@ hipError_t launch_attend_select(const Shape& s, const uint16_t* Q, const uint16_
   P.sel_scores = scores;
   P.sel_packed = ws ? reinterpret_cast<const float*>(ws + ws_scores_off(s)) : nullptr;
   P.sel_trigger = trigger ? trigger : ws + ws_trigger_off(s);
+  if (s.d == 256) return launch_t<256, true>(P, stream);
   return s.d == 128 ? launch_t<128, true>(P, stream) : launch_t<64, true>(P, stream);
 }
 

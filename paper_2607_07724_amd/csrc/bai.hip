@@ -30,7 +30,6 @@
 namespace ugbs {
 namespace {
 
-constexpr int kRho = 2;
 constexpr int kBaiUnits = 4;   // query heads of one tile per workgroup (one wave each)
 constexpr int kBaiSlots = UGBS_MAX_BLOCKS / 64;
 constexpr int kHeadThreads = 256;
@@ -87,7 +86,7 @@ __global__ void __launch_bounds__(64 * kBaiUnits) bai_tile_kernel(TileParams P) 
   const int nf = (t == 0) ? 1 : 2;
   const int nc = (t >= 1) ? t - 1 : 0;
   const int m = s.k - nf;              // kept non-forced slots
-  const int Rp = kRho * s.k - nf;      // non-forced slots after expansion
+  const int Rp = s.W - nf;             // non-forced slots after expansion (rho k - |F|)
   if (nc < Rp + 1 || nc <= m) {        // outside the diagnostic mask (uniform: depends on t)
     if (w < n_act && lane == 0) {
       const float nan = __builtin_nanf("");
@@ -127,6 +126,7 @@ __global__ void __launch_bounds__(64 * kBaiUnits) bai_tile_kernel(TileParams P) 
     for (int j = lane; j < Rp; j += 64)
       if (j != m - 1) dm = fminf(dm, cs(j) - cs(j + 1));
     d2 = wave_min_f(dm);
+    if (Rp < 2) d2 = __builtin_nanf("");  // no spacing besides the cut (rho = 1, m = 1)
     {
       const float c0 = cs(0), cm1 = cs(m - 1), cm = cs(m), cR = cs(Rp);
       g = cm1 - cm;
@@ -474,7 +474,7 @@ __global__ void __launch_bounds__(kHeadThreads) bai_head_kernel(HeadParams P) {
   if (have_tau) {
     double eb = __builtin_huge_val();
     if (!__builtin_isinf(chi)) {
-      const double x = (double)(kRho - 1) * s.k * (double)p05;
+      const double x = (double)(s.rho - 1) * s.k * (double)p05;
       eb = chi + (1.0 + chi) * exp(-(x * x) / (4.0 * tb * tb));
     }
     const double bandt = sqrt(2.0) * beta * gamma / tb * std_normal_pdf(gamma * (1.0 - beta) / (sqrt(2.0) * tb));
@@ -512,12 +512,12 @@ hipError_t launch_bai_tiles(const Shape& s, const float* scores, const float* ta
   // sort buffer for the top R' + 1 (a power of two of 8-byte entries; only
   // tiles with R' + 1 <= |C(t)| <= N_B - 2 are sorted), reused for the
   // masked score row (N_B floats, padded to a multiple of 8)
-  const int r1 = kRho * s.k - 1;
+  const int r1 = s.W - 1;
   int n2 = 2;
   while (n2 < r1 && n2 < s.NB) n2 <<= 1;
   const int sel = 8 * n2 > 4 * (s.NB + 8) ? 8 * n2 : 4 * (s.NB + 8);
   P.sel_bytes = (sel + 15) & ~15;
-  P.top_bytes = (8 * (kRho * s.k) + 15) & ~15;
+  P.top_bytes = (8 * s.W + 15) & ~15;
   const size_t smem = (size_t)kBaiUnits * (P.sel_bytes + P.top_bytes);
   if (smem > 65536) {
     const hipError_t e = hipFuncSetAttribute((const void*)bai_tile_kernel,

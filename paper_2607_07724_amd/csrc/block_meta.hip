@@ -113,7 +113,12 @@ hipError_t launch_block_meta(const Shape& s, const uint16_t* K, uint16_t* meta,
   const long n_items = (long)s.B * s.Hkv * s.NB * (s.d / 8);
   const int threads = 256;
   const unsigned grid = (unsigned)((n_items + threads - 1) / threads);
-  if (s.d == 128) {
+  if (s.d == 256) {
+    if (s.backbone == UGBS_QUEST)
+      block_meta_kernel<256, true><<<grid, threads, 0, stream>>>(K, meta, n_items, s.N);
+    else
+      block_meta_kernel<256, false><<<grid, threads, 0, stream>>>(K, meta, n_items, s.N);
+  } else if (s.d == 128) {
     if (s.backbone == UGBS_QUEST)
       block_meta_kernel<128, true><<<grid, threads, 0, stream>>>(K, meta, n_items, s.N);
     else

@@ -215,14 +215,20 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
   double rough = 0.0;
   if (nc > 0) {
     // ---- A operand: this wave's 64 query rows (Quest: [q- | q+]) ----------
-    bf16x8 a[4][KS];
+    // d = 256 Quest: the split pair would take 256 registers per lane, so the
+    // raw q rows stay in registers and are split per MFMA (two bit masks)
+    constexpr bool FLY = QUEST && D >= 256;
+    constexpr int KA = FLY ? D / 32 : KS;
+    bf16x8 a[4][KA];
     const uint16_t* qtile = P.Q + (((size_t)gr.b * s.H + h) * s.N + (size_t)t * kBlock) * D;
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) {
       const uint16_t* qrow = qtile + (size_t)(16 * rt + c16) * D;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        if constexpr (QUEST) {
+      for (int ks = 0; ks < KA; ++ks) {
+        if constexpr (FLY) {
+          a[rt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g));
+        } else if constexpr (QUEST) {
           const int kk = (ks % (D / 32)) * 32 + 8 * g;
           const uint4 v = *reinterpret_cast<const uint4*>(qrow + kk);
           a[rt][ks] = as_bf16x8(ks < D / 32 ? neg_part(v) : pos_part(v));
@@ -281,12 +287,28 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
         f32x4 acc[4];
 #pragma unroll
         for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if constexpr (FLY) {
+          // min(q,0) . kmin + max(q,0) . kmax, k-step by k-step
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 b = as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(c16, 4 * ks + g)));
+          for (int ks = 0; ks < KA; ++ks) {
+            const bf16x8 bmin = as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(c16, 4 * ks + g)));
+            const bf16x8 bmax =
+                as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(c16, 4 * (ks + D / 32) + g)));
 #pragma unroll
-          for (int rt = 0; rt < 4; ++rt)
-            acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][ks], b, acc[rt], 0, 0, 0);
+            for (int rt = 0; rt < 4; ++rt) {
+              const uint4 raw = __builtin_bit_cast(uint4, a[rt][ks]);
+              acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(neg_part(raw)), bmin, acc[rt], 0, 0, 0);
+              acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(pos_part(raw)), bmax, acc[rt], 0, 0, 0);
+            }
+          }
+        } else {
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            const bf16x8 b = as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(c16, 4 * ks + g)));
+#pragma unroll
+            for (int rt = 0; rt < 4; ++rt)
+              acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][ks], b, acc[rt], 0, 0, 0);
+          }
         }
         const int pos = kChunk * c + c16;
         if constexpr (ROUGH) {
@@ -347,8 +369,11 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
   const int nc = (t >= 1) ? t - 1 : 0;
   const int m = s.k - nf;
   const int W = s.W;
-  // without idx_sorted only sigma is wanted: the m + 1 largest suffice
-  const int R = P.idx_sorted ? min(W - nf, nc) : min(m + 1, nc);
+  // the row lists R_out = min(W - |F|, |C|) candidates; sigma needs the m + 1
+  // largest, more than the row holds when rho = 1; without idx_sorted only
+  // sigma is wanted
+  const int R_out = min(W - nf, nc);
+  const int R = P.idx_sorted ? min(max(W - nf, m + 1), nc) : min(m + 1, nc);
   uint64_t* s_sel = reinterpret_cast<uint64_t*>(smem + w * P.wave_lds);
   const float* src = PACKED ? P.scratch + packed_row(b * s.H + h, t, s.T) : P.scores_in + row * s.NB + 1;
 
@@ -487,7 +512,7 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
     int v;
     if (p < nf)
       v = (p == 0) ? 0 : t;
-    else if (p - nf < R)
+    else if (p - nf < R_out)
       v = 1 + (int)(0xffffffffu - (uint32_t)(s_sel[p - nf] & 0xffffffffu));
     else
       v = s.NB;
@@ -542,6 +567,9 @@ hipError_t launch_select(const SelParams& P, hipStream_t stream) {
 template <int OUT>
 hipError_t launch_score_d(const SelParams& P, hipStream_t stream) {
   const Shape& s = P.s;
+  if (s.d == 256)
+    return s.backbone == UGBS_QUEST ? launch_score<256, true, OUT>(P, stream)
+                                    : launch_score<256, false, OUT>(P, stream);
   if (s.d == 128)
     return s.backbone == UGBS_QUEST ? launch_score<128, true, OUT>(P, stream)
                                     : launch_score<128, false, OUT>(P, stream);

@@ -17,7 +17,7 @@ typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 
 // Validated problem with derived sizes; passed by value to launchers.
 struct Shape {
-  int B, H, Hkv, G, N, d, NB, T, k, W, backbone;
+  int B, H, Hkv, G, N, d, NB, T, k, W, backbone, rho;  // W = rho k
   double q;
   float scale;
 };

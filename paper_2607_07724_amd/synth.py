@@ -7,8 +7,9 @@ that both sides read byte-identical inputs.
 
 The workload shapes follow the attention shapes of the models the paper
 evaluates (Qwen2.5-7B-Instruct-1M: 28 query / 4 kv heads, d_head 128;
-Mistral-Nemo-2407: 32 / 8, d_head 128; Section 4.1) at the context lengths of
-its speed study (32K-128K, Table 3).  Real activations are not available, so
+Mistral-Nemo-2407: 32 / 8, d_head 128; the full-attention layers of
+Qwen3.6-35B-A3B: 16 / 2, d_head 256, with per-head QK-Norm; Section 4.1) at
+the context lengths of its speed study (32K-128K, Table 3).  Real activations are not available, so
 Gaussian queries/values and block-offset or cluster-mixture keys stand in for
 them, with needle keys that imitate needle-in-a-haystack retrieval.
 
@@ -45,6 +46,8 @@ class Workload:
     dup_pairs: bool = False
     layers: int = 1
     base_seed: int = 20260000
+    rho: int = 2            # expansion factor (kv_idx rows hold rho k slots)
+    qk_norm: bool = False   # per-head RMS normalisation of query and key rows
 
     @property
     def NB(self) -> int:
@@ -55,7 +58,7 @@ class Workload:
         return self.N // BLOCK
 
     def seed(self, layer: int = 0) -> int:
-        idx = {"C1": 1, "C2": 2, "C3": 3, "C4": 4, "C5": 5}.get(self.name.split("_")[0], 9)
+        idx = {"C1": 1, "C2": 2, "C3": 3, "C4": 4, "C5": 5, "C6": 6}.get(self.name.split("_")[0], 9)
         return self.base_seed + 100 * idx + layer
 
     def replace(self, **kw) -> "Workload":
@@ -75,6 +78,9 @@ WORKLOADS = {
     "C4": Workload("C4", 1, 32, 8, 128, 131072, 64, 0.1, QUEST, "mixture", needles=32),
     # 28-layer stack at Qwen2.5-7B-1M shape, 128K, k 64, q 0.1, 32 needles / layer
     "C5": Workload("C5", 1, 28, 4, 128, 131072, 64, 0.1, QUEST, "mixture", needles=32, layers=28),
+    # Qwen3.6-35B-A3B full-attention layer: 16 q / 2 kv heads, d 256, QK-normed
+    # rows, 128K, K-mean (the backbone that wins on this model), k 33, q 0.4
+    "C6": Workload("C6", 1, 16, 2, 256, 131072, 33, 0.4, KMEAN, "offset", needles=32, qk_norm=True),
 }
 
 
@@ -93,8 +99,17 @@ def _rng(seed: int, tensor: int, b: int, h: int) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, tensor, b, h])))
 
 
-def _normal_head(seed, tensor, b, h, N, d):
-    return bf16_bits(_rng(seed, tensor, b, h).standard_normal((N, d), dtype=np.float32))
+def _rms_norm(x: np.ndarray) -> np.ndarray:
+    """Row-wise RMS normalisation with unit gain (the per-head QK-Norm of
+    Qwen3-style attention), fp32."""
+    x = np.asarray(x, np.float32)
+    ms = np.mean(x.astype(np.float64) ** 2, axis=-1, keepdims=True)
+    return (x / np.sqrt(ms + 1e-6)).astype(np.float32)
+
+
+def _normal_head(seed, tensor, b, h, N, d, norm=False):
+    x = _rng(seed, tensor, b, h).standard_normal((N, d), dtype=np.float32)
+    return bf16_bits(_rms_norm(x) if norm else x)
 
 
 def _key_head(w: Workload, seed, b, h):
@@ -110,15 +125,15 @@ def _key_head(w: Workload, seed, b, h):
             off[2] *= np.float32(4.0)
             off[3] *= np.float32(3.0)
             off[6] *= np.float32(3.0)
-        k = noise.reshape(NB, BLOCK, d) + off[:, None, :]
-        return bf16_bits(k.reshape(N, d))
+        k = (noise.reshape(NB, BLOCK, d) + off[:, None, :]).reshape(N, d)
+        return bf16_bits(_rms_norm(k) if w.qk_norm else k)
     if w.keys == "mixture":
         gc = _rng(seed, _TCENT, b, h)
         centres = gc.standard_normal((64, d), dtype=np.float32)
         ga = _rng(seed, _TASSIGN, b, h)
         assign = ga.integers(0, 64, size=N)
         k = centres[assign] + np.float32(0.3) * noise
-        return bf16_bits(k)
+        return bf16_bits(_rms_norm(k) if w.qk_norm else k)
     raise ValueError(w.keys)
 
 
@@ -151,7 +166,7 @@ def generate(w: Workload, layer: int = 0, threads: int = 8) -> Inputs:
     def do(item):
         kind, b, h = item
         if kind == "q":
-            Q[b, h] = _normal_head(seed, _TQ, b, h, N, d)
+            Q[b, h] = _normal_head(seed, _TQ, b, h, N, d, norm=w.qk_norm)
         elif kind == "v":
             V[b, h] = _normal_head(seed, _TV, b, h, N, d)
         else:
@@ -186,7 +201,10 @@ def generate(w: Workload, layer: int = 0, threads: int = 8) -> Inputs:
         blk = int(gp.integers(1, t))          # a non-forced visible block
         j = blk * BLOCK + int(gp.integers(0, BLOCK))
         qv = bf16_to_f32(Q[b, h, i])
-        key = np.float32(8.0) * qv / np.float32(np.linalg.norm(qv.astype(np.float64)))
+        if w.qk_norm:   # a normalised key can only align with the query, not grow
+            key = _rms_norm(qv[None, :])[0]
+        else:
+            key = np.float32(8.0) * qv / np.float32(np.linalg.norm(qv.astype(np.float64)))
         K[b, h // G, j] = bf16_bits(key)
         needles.append((b, h, i, j))
         if w.needle_pairs:

@@ -68,7 +68,10 @@ BAD = [
     (dict(seq_len=1000), "UGBS_ERR_SHAPE"),
     (dict(seq_len=0), "UGBS_ERR_SHAPE"),
     (dict(seq_len=64 * 4096), "UGBS_ERR_SHAPE"),
-    (dict(reserved=1), "UGBS_ERR_SHAPE"),
+    (dict(rho=9), "UGBS_ERR_BUDGET"),
+    (dict(rho=-1), "UGBS_ERR_BUDGET"),
+    (dict(rho=8, k_budget=513), "UGBS_ERR_BUDGET"),
+    (dict(head_dim=512), "UGBS_ERR_SHAPE"),
     (dict(k_budget=2), "UGBS_ERR_BUDGET"),
     (dict(k_budget=2049), "UGBS_ERR_BUDGET"),
     (dict(q=-0.01), "UGBS_ERR_Q"),
@@ -261,3 +264,16 @@ def test_diagnostics_record_layout_matches_header(tmp_path):
         assert int(out["t." + n]) == td.fields[n][1], n
     for n in head_fields:
         assert int(out["h." + n]) == hd.fields[n][1], n
+
+
+def test_rho_and_head_dim_256_accepted():
+    """rho = 0 means 2; d = 256 and rho in 1..8 with rho k <= 4096 are valid
+    problems (validated through the workspace query, which launches nothing)."""
+    L = ugbs.lib()
+    for kw in (dict(rho=0), dict(rho=1), dict(rho=8, k_budget=512), dict(head_dim=256), dict(rho=3)):
+        p = good(**kw)
+        assert L.ugbs_workspace_bytes(ctypes.byref(p)) > 0, kw
+    assert ugbs.Problem.make(1, 2, 1, 1024, 64, 5, 0.1, rho=3).W == 15
+    p = good()
+    p.rho = 0
+    assert p.W == 2 * p.k_budget

@@ -49,7 +49,7 @@ def sample_units(w, n, seed):
 def run_full(w, layer=0, units_n=20):
     torch = __import__("torch")
     inp = synth.generate(w, layer=layer, threads=16)
-    p = ugbs.Problem.make(w.B, w.H, w.Hkv, w.N, w.d, w.k, w.q, w.backbone)
+    p = ugbs.Problem.make(w.B, w.H, w.Hkv, w.N, w.d, w.k, w.q, w.backbone, rho=w.rho)
     Q, K, V = dev_bf16(inp.Q), dev_bf16(inp.K), dev_bf16(inp.V)
     bufs = ugbs.Buffers(p)
     so = torch.empty((w.B, w.H, w.T, w.NB), dtype=torch.float32, device="cuda")
@@ -86,7 +86,7 @@ def check_all(r):
         assert np.all(err <= bound), (b, h, t, float((err / bound).max()))
 
     # ---- selection of sampled rows given the oracle's scores: bit-exact
-    ridx, rsig = oracle.select(S, k, t_of_row=units[:, 2])
+    ridx, rsig = oracle.select(S, k, t_of_row=units[:, 2], rho=w.rho)
     sin = torch.zeros((w.B, w.H, T, NB), dtype=torch.float32, device="cuda")
     for i, (b, h, t) in enumerate(units):
         sin[b, h, t] = torch.from_numpy(S[i]).cuda()
@@ -139,7 +139,7 @@ def check_all(r):
     assert np.all(kv[:, :, 1:, 1] == np.arange(1, T)[None, None, :])
 
     # ---- attention on the oracle's kept lists of sampled rows
-    for width in (k, 2 * k):
+    for width in (k, w.rho * k):
         rows = ridx.copy()
         rows[:, width:] = NB
         kvt = torch.full_like(bufs.kv_idx, NB)
@@ -156,7 +156,7 @@ def check_all(r):
     print(f"{w.name}: {len(units)} sampled units, near-tie exemptions {exempt}")
 
 
-@pytest.mark.parametrize("name", ["C2", "C3", "C4"])
+@pytest.mark.parametrize("name", ["C2", "C3", "C4", "C6"])
 def test_full_size_workload(name):
     r = run_full(synth.WORKLOADS[name])
     check_all(r)

@@ -39,6 +39,16 @@ CASES = {
                                      base_seed=33),
     "kmean_d64_mha": synth.Workload("M4", 1, 3, 3, 64, 1344, 3, 0.5, synth.KMEAN, "offset",
                                     base_seed=34),
+    # d 256 with QK-normed rows (the Qwen3.6 full-attention shape, scaled down)
+    "kmean_d256_qknorm": synth.Workload("M5", 1, 4, 2, 256, 2048, 5, 0.4, synth.KMEAN, "offset",
+                                        needles=4, qk_norm=True, base_seed=35),
+    "quest_d256_rho4": synth.Workload("M6", 1, 4, 1, 256, 1536, 4, 0.3, synth.QUEST, "mixture",
+                                      rho=4, base_seed=36),
+    # expansion factors other than 2
+    "kmean_d128_rho3": synth.Workload("M7", 1, 4, 2, 128, 2048, 4, 0.3, synth.KMEAN, "offset",
+                                      rho=3, base_seed=37),
+    "quest_d64_rho1": synth.Workload("M8", 1, 2, 1, 64, 1024, 4, 0.5, synth.QUEST, "mixture",
+                                     rho=1, base_seed=38),
 }
 
 
@@ -61,8 +71,8 @@ def case(name):
     inp = synth.generate(w, threads=8)
     meta = oracle.block_meta(w.backbone, inp.K)
     S = oracle.tile_scores(w.backbone, inp.Q, meta, w.Hkv)
-    idx, sig = oracle.select(S, w.k)
-    kv, sb, tau, trig = oracle.route(sig, idx, w.k, w.q)
+    idx, sig = oracle.select(S, w.k, rho=w.rho)
+    kv, sb, tau, trig = oracle.route(sig, idx, w.k, w.q, rho=w.rho)
     r = dict(w=w, inp=inp, meta=meta, S=S, idx=idx, sig=sig, kv=kv, sb=sb, tau=tau, trig=trig)
     _cache[name] = r
     return r
@@ -70,7 +80,7 @@ def case(name):
 
 def problem(w, k=None, q=None):
     return ugbs.Problem.make(w.B, w.H, w.Hkv, w.N, w.d, w.k if k is None else k,
-                             w.q if q is None else q, w.backbone)
+                             w.q if q is None else q, w.backbone, rho=w.rho)
 
 
 def gpu_inputs(inp):
@@ -117,9 +127,11 @@ def test_selection_given_oracle_scores_is_bit_exact(name):
     w = c["w"]
     Q = dev_bf16(c["inp"].Q)
     for k in sorted({3, w.k, min(2 * w.k, w.NB), w.NB}):
+        if w.rho * k > ugbs.MAX_KV_WIDTH:
+            continue
         p = problem(w, k=k)
         idx, sig, _ = _select_gpu(w, p, Q, c["meta"], scores_in=c["S"])
-        ridx, rsig = oracle.select(c["S"], k)
+        ridx, rsig = oracle.select(c["S"], k, rho=w.rho)
         assert np.array_equal(idx, ridx), f"k={k}"
         assert np.array_equal(sig.view(np.uint32), rsig.view(np.uint32)), f"k={k}"
 
@@ -200,7 +212,7 @@ def test_route_given_oracle_sigma_is_bit_exact(name, q, in_place):
     w = c["w"]
     qq = w.q if q is None else q
     p = problem(w, q=qq)
-    kv_ref, sb_ref, tau_ref, trig_ref = oracle.route(c["sig"], c["idx"], w.k, qq)
+    kv_ref, sb_ref, tau_ref, trig_ref = oracle.route(c["sig"], c["idx"], w.k, qq, rho=w.rho)
     sig = dev(c["sig"])
     idx = dev(c["idx"])
     kv = idx if in_place else torch.full_like(idx, -7)
@@ -314,7 +326,7 @@ def test_end_to_end_against_oracle(name):
                 assert abs(float(c["sb"][b, t]) - float(c["tau"][b])) <= 1e-3, (b, t)
                 exempt += 1
             for h in range(w.H):
-                width = 2 * k if g["trig"][b, t] else k
+                width = w.rho * k if g["trig"][b, t] else k
                 orc_row = c["idx"][b, h, t].copy()
                 orc_row[width:] = NB
                 ok, nd = near_tie_ok(g["kv"][b, h, t], orc_row, c["S"][b, h, t], t, NB)
@@ -355,8 +367,8 @@ def test_tiny_sequences(N):
     g = _pipeline_gpu(w, inp)
     meta = oracle.block_meta(w.backbone, inp.K)
     S = oracle.tile_scores(w.backbone, inp.Q, meta, w.Hkv)
-    idx, sig = oracle.select(S, w.k)
-    kv, *_ = oracle.route(sig, idx, w.k, w.q)
+    idx, sig = oracle.select(S, w.k, rho=w.rho)
+    kv, *_ = oracle.route(sig, idx, w.k, w.q, rho=w.rho)
     assert np.array_equal(g["kv"], kv)          # no candidates to tie on
     ref = oracle.attend(inp.Q, inp.K, inp.V, kv_idx=kv)
     mx, rms = attention_error(g["O"], ref)
