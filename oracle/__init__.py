@@ -36,6 +36,8 @@ def lib():
         L.orc_attend.argtypes = [i32, i32, i32, i32, f64, P, P, P, P, i32, i32, i64, P, P, i32]
         L.orc_row_roughness.argtypes = [i32, i32, i32, i32, i32, P, P, i64, P, P, i32]
         L.orc_row_roughness.restype = ctypes.c_int
+        L.orc_row_scores.argtypes = [i32, i32, i32, i32, i32, P, P, i64, P, P, i32]
+        L.orc_row_scores.restype = ctypes.c_int
         L.orc_bf16_round.argtypes = [f64]
         L.orc_bf16_round.restype = ctypes.c_uint16
         for f in ("orc_block_meta", "orc_tile_scores", "orc_select", "orc_route", "orc_attend"):
@@ -186,6 +188,62 @@ def row_roughness(backbone, Q, meta, Hkv, units=None, nthreads=None):
     assert rc == 0
     terms = 63 * np.maximum(units[:, 2].astype(np.int64) - 1, 0)
     return out, terms
+
+
+def row_scores(backbone, Q, meta, Hkv, units=None, nthreads=None):
+    """A.2 per row: for each unit (b, h, t) the [64, N_B] fp32 scores of the
+    tile's query rows against the candidate blocks C(t) (fp64, rounded to
+    fp32; -inf elsewhere).  Returns [n_units, 64, N_B] ([B, H, T, 64, N_B]
+    with units=None)."""
+    Q = _c(Q, np.uint16)
+    meta = _c(meta, np.uint16)
+    B, H, N, d = Q.shape
+    T = N // BLOCK
+    full = units is None
+    if full:
+        units = all_units(B, H, T)
+    units = _c(np.asarray(units, np.int32), np.int32)
+    out = np.empty((units.shape[0], BLOCK, T), np.float32)
+    rc = lib().orc_row_scores(backbone, H, Hkv, N, d, _ptr(Q), _ptr(meta), units.shape[0],
+                              _ptr(units), _ptr(out), nthreads or default_threads())
+    assert rc == 0
+    return out.reshape(B, H, T, BLOCK, T) if full else out
+
+
+def select_rows(rows, t_of_unit, k, rho=2, trig_of_unit=None):
+    """Per-row selection scattered into a per-tile bitmap (the per-row variant
+    the Limitations of Section 4 name; Section 3.2 describes the per-tile
+    rule it refines).  For each unit with tile t and each of its 64 rows:
+    the forced blocks F = [0] (t = 0) or [0, t] and the row's R best
+    candidates of C(t) by (row score descending, lower block first, -0 ==
+    +0), R = (trigger ? rho k : k) - |F|, all of C(t) when fewer; the tile's
+    set is the union over its rows.
+
+    rows [n_units, 64, N_B] fp32; returns [n_units, ceil(N_B / 32)] uint32
+    words (bit b of word b // 32 set = block b attended)."""
+    rows = np.asarray(rows, np.float32)
+    n, R64, NB = rows.shape
+    nw = (NB + 31) // 32
+    out = np.zeros((n, nw), np.uint32)
+    for u in range(n):
+        t = int(t_of_unit[u])
+        nf = 1 if t == 0 else 2
+        nc = max(t - 1, 0)
+        trig = bool(trig_of_unit[u]) if trig_of_unit is not None else False
+        R = min((rho * k if trig else k) - nf, nc)
+        keep = {0} | ({t} if t > 0 else set())
+        for r in range(R64):
+            cand = [(float(rows[u, r, b]) + 0.0, b) for b in range(1, t)]   # -0 -> +0
+            cand.sort(key=lambda x: (-x[0], x[1]))
+            keep |= {b for _, b in cand[:R]}
+        for b in keep:
+            out[u, b // 32] |= np.uint32(1 << (b % 32))
+    return out
+
+
+def bitmap_blocks(words, NB):
+    """The attended blocks of one bitmap row, ascending."""
+    return [b for b in range(NB) if (int(words[b // 32]) >> (b % 32)) & 1]
 
 
 def population(T, k):

@@ -494,4 +494,57 @@ int orc_row_roughness(int backbone, int H, int Hkv, int N, int d, const uint16_t
   return 0;
 }
 
+/* ------------------------------------------------------------------ */
+/* Per-row block scores (A.2 before the max over the tile's rows), for   */
+/* the per-row selection variant (Section 3.2 and the Limitations of    */
+/* Section 4)                                                           */
+/* ------------------------------------------------------------------ */
+/* For each requested unit (b, h, t): out[unit][r][blk] = the fp64 score of
+ * query row r of tile t against block blk, rounded to fp32, for blk in
+ * C(t) = {1..t-1}; -inf elsewhere. */
+typedef struct {
+  int backbone, H, Hkv, N, d;
+  const uint16_t* Q;
+  const uint16_t* meta;
+  const int32_t* units;
+  float* out;
+} rows_ctx;
+
+static void rows_item(long u, void* vctx) {
+  rows_ctx* c = (rows_ctx*)vctx;
+  int NB = c->N / ORC_BLOCK, d = c->d, G = c->H / c->Hkv;
+  int b = c->units[3 * u], h = c->units[3 * u + 1], t = c->units[3 * u + 2];
+  int kvh = h / G;
+  float* out = c->out + (size_t)u * ORC_BLOCK * NB;
+  for (long x = 0; x < (long)ORC_BLOCK * NB; ++x) out[x] = -INFINITY;
+  const uint16_t* qb = c->Q + (((size_t)b * c->H + h) * c->N + (size_t)t * ORC_BLOCK) * d;
+  int width = (c->backbone == ORC_KMEAN) ? 1 : 2;
+  for (int blk = 1; blk <= t - 1; ++blk) {
+    const uint16_t* m = c->meta + (((size_t)b * c->Hkv + kvh) * NB + blk) * width * d;
+    for (int r = 0; r < ORC_BLOCK; ++r) {
+      const uint16_t* qr = qb + (size_t)r * d;
+      double s = 0.0;
+      if (c->backbone == ORC_KMEAN) {
+        for (int e = 0; e < d; ++e) s += bf16_val(qr[e]) * bf16_val(m[e]);
+      } else {
+        for (int e = 0; e < d; ++e) {
+          double a = bf16_val(qr[e]) * bf16_val(m[d + e]);
+          double z = bf16_val(qr[e]) * bf16_val(m[e]);
+          s += (a > z) ? a : z;
+        }
+      }
+      out[(size_t)r * NB + blk] = (float)s;
+    }
+  }
+}
+
+int orc_row_scores(int backbone, int H, int Hkv, int N, int d, const uint16_t* Q,
+                   const uint16_t* meta, long n_units, const int32_t* units, float* out,
+                   int nthreads) {
+  if (N % ORC_BLOCK || H % Hkv) return -1;
+  rows_ctx c = {backbone, H, Hkv, N, d, Q, meta, units, out};
+  orc_parallel(n_units, nthreads, rows_item, &c);
+  return 0;
+}
+
 uint16_t orc_bf16_round(double x) { return bf16_round(x); }

@@ -521,3 +521,110 @@ def test_rho_expansion(rho):
     n, n_trig = int(P.sum()), math.ceil(0.25 * int(P.sum()))
     extra = int(np.sum((np.minimum(rho * k, V) - rho * k)[P & ~big & trig[0].astype(bool)]))
     assert slots[:, P].sum(axis=1).tolist() == [k * n + (rho - 1) * k * n_trig + extra] * H
+
+
+# ---------------------------------------------------------------- per-row selection variant
+
+@pytest.mark.parametrize("backbone", [oracle.KMEAN, oracle.QUEST])
+def test_row_scores_are_the_contraction_and_max_to_the_tile_score(backbone):
+    inp = small_inputs(keys="mixture", N=384)
+    meta = oracle.block_meta(backbone, inp.K)
+    R = oracle.row_scores(backbone, inp.Q, meta, inp.K.shape[1])          # [B,H,T,64,T]
+    S = oracle.tile_scores(backbone, inp.Q, meta, inp.K.shape[1])
+    B, H, N, d = inp.Q.shape
+    G, T = H // inp.K.shape[1], N // BLK
+    Qd = f32(inp.Q).astype(np.float64)
+    for h in range(H):
+        kv = h // G
+        if backbone == oracle.KMEAN:
+            ref = Qd[0, h] @ f32(meta[0, kv, :, 0]).astype(np.float64).T
+        else:
+            lo, hi = (f32(meta[0, kv, :, i]).astype(np.float64) for i in (0, 1))
+            ref = np.maximum(Qd[0, h], 0) @ hi.T + np.minimum(Qd[0, h], 0) @ lo.T
+        for t in range(T):
+            got = R[0, h, t]
+            np.testing.assert_allclose(got[:, 1:t], ref[64 * t:64 * t + 64, 1:t].astype(np.float32),
+                                       rtol=1e-6, atol=1e-6)
+            assert np.all(np.isneginf(got[:, [0] + list(range(t, T))]))
+            # rounding is monotone: max over rows of the rounded scores is the tile score
+            if t >= 2:
+                assert np.array_equal(got[:, 1:t].max(axis=0), S[0, h, t, 1:t])
+
+
+def _row_oracle_brute(rows, t, k, rho, trig):
+    nf = 1 if t == 0 else 2
+    nc = max(t - 1, 0)
+    R = min((rho * k if trig else k) - nf, nc)
+    keep = {0} | ({t} if t else set())
+    for r in range(rows.shape[0]):
+        c = list(range(1, t))
+        # the kept set is the unique R-subset dominating every dropped candidate
+        best = None
+        import itertools
+        for sub in itertools.combinations(c, R):
+            rest = [b for b in c if b not in sub]
+            key = lambda b: (float(rows[r, b]) + 0.0, -b)
+            if all(key(a) > key(b) for a in sub for b in rest):
+                assert best is None
+                best = set(sub)
+        assert best is not None or R == 0
+        keep |= best or set()
+    return keep
+
+
+def test_select_rows_brute_force_ties_and_signed_zeros():
+    g = np.random.default_rng(12)
+    T = 9
+    rows = np.round(g.standard_normal((6, 64, T)) * 1.5).astype(np.float32)
+    rows[g.random(rows.shape) < 0.2] = np.float32(-0.0)
+    rows[:, 3:, :] = rows[:, :3, :].repeat(21, axis=1)[:, :61, :]      # repeated rows
+    ts = np.array([0, 2, 5, 8, 8, 7])
+    trig = np.array([0, 1, 0, 0, 1, 1])
+    for k, rho in ((3, 2), (4, 2), (3, 3)):
+        got = oracle.select_rows(rows, ts, k, rho, trig)
+        for u in range(6):
+            want = _row_oracle_brute(rows[u, :4], ts[u], k, rho, trig[u])          # 4 distinct rows
+            assert set(oracle.bitmap_blocks(got[u], T)) == want, (k, rho, u)
+
+
+def test_select_rows_on_identical_rows_is_the_tile_selection():
+    """All 64 rows equal: each row's ranking is the tile's, so the union is
+    the kept prefix of the per-tile kv_idx row (triggered: rho k slots)."""
+    g = np.random.default_rng(13)
+    T, k = 40, 4
+    S = np.full((1, 1, T, T), -np.inf, np.float32)
+    for t in range(2, T):
+        S[0, 0, t, 1:t] = g.standard_normal(t - 1).astype(np.float32)
+    rows = np.repeat(S[0, 0][:, None, :], 64, axis=1)                        # [T, 64, T]
+    for rho in (1, 2, 3):
+        idx, sig = oracle.select(S, k, rho=rho)
+        for trig_val in (0, 1):
+            trig = np.full(T, trig_val)
+            got = oracle.select_rows(rows, np.arange(T), k, rho, trig)
+            for t in range(T):
+                width = rho * k if trig_val else k
+                want = {int(b) for b in idx[0, 0, t, :width] if b != T}
+                assert set(oracle.bitmap_blocks(got[t], T)) == want
+
+
+def test_select_rows_union_covers_row_argmax_and_tile_top():
+    inp = small_inputs(keys="mixture", N=512)
+    meta = oracle.block_meta(oracle.QUEST, inp.K)
+    R = oracle.row_scores(oracle.QUEST, inp.Q, meta, inp.K.shape[1])
+    S = oracle.tile_scores(oracle.QUEST, inp.Q, meta, inp.K.shape[1])
+    B, H, T = R.shape[:3]
+    units = oracle.all_units(B, H, T)
+    rows = R.reshape(-1, 64, T)
+    bits = oracle.select_rows(rows, units[:, 2], 3, 2, None)
+    idx, _ = oracle.select(S, 3)
+    for u, (b, h, t) in enumerate(units):
+        got = set(oracle.bitmap_blocks(bits[u], T))
+        if t >= 2:
+            for r in range(64):
+                assert int(np.argmax(rows[u, r, 1:t])) + 1 in got      # every row's best block
+            assert int(idx[b, h, t, 2 if t else 1]) in got               # the tile's best candidate
+        assert {0, t} <= got and max(got) <= t
+    # k >= N_B: every visible block
+    bits = oracle.select_rows(rows, units[:, 2], T, 2, None)
+    for u, (b, h, t) in enumerate(units):
+        assert oracle.bitmap_blocks(bits[u], T) == list(range(t + 1))
