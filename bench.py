@@ -203,6 +203,45 @@ def main():
     log(f"fused: {fused_ms:.3f} ms/step; stages {np.round(fst, 4).tolist()}; output identical: {same}")
     del fb
 
+    # per-row selection into tile bitmaps (union over each tile's rows)
+    rb = ugbs.Buffers(p, device=dev)
+    Or = torch.empty_like(Q)
+    bm = torch.empty((w.B, w.H, w.T, ugbs.bitmap_words(p)), dtype=torch.int32, device=dev)
+
+    def step_rows(ev=None):
+        rec = (lambda i: ev[i].record(stream)) if ev is not None else (lambda i: None)
+        rec(0)
+        ugbs.ugbs_block_meta(p, K, rb.meta)
+        ugbs.ugbs_score_select(p, Q, rb.meta, None, rb.sigma, workspace=rb.workspace)
+        ugbs.ugbs_route(p, rb.sigma, None, None, rb.workspace, rb.sigma_bar, rb.tau, rb.trigger)
+        rec(1)
+        ugbs.ugbs_select_rows(p, rb.trigger, bm, Q=Q, meta=rb.meta)
+        rec(2)
+        ugbs.ugbs_attend_bitmap(p, Q, K, V, bm, Or)
+        rec(3)
+
+    for i in range(a.warmup):
+        step_rows()
+    torch.cuda.synchronize(dev)
+    revs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(a.steps)]
+    t0 = time.perf_counter()
+    for i in range(a.steps):
+        step_rows(revs[i])
+    torch.cuda.synchronize(dev)
+    rows_ms = 1e3 * (time.perf_counter() - t0) / a.steps
+    rst = np.array([[revs[i][j].elapsed_time(revs[i][j + 1]) for j in range(3)] for i in range(a.steps)]).mean(axis=0)
+    bmh = bm.cpu().numpy().view(np.uint32)
+    kept_rows = np.unpackbits(bmh.view(np.uint8), axis=-1).reshape(w.B, w.H, w.T, -1).sum(axis=-1)
+    kv_rows = np.full((w.B, w.H, w.T, 1), w.NB, np.int32)   # flop count from the bitmaps' block sets
+    f_rows = 0.0
+    tt = np.arange(w.T)[None, None, :]
+    n_full = kept_rows - 1                                   # every set is [.., t]: t is the diagonal
+    f_rows = 4.0 * w.d * float(n_full.sum() * 64 * 64 + kept_rows.size * (64 * 65 // 2))
+    rows_hits = [int((int(bmh[b, h, i // 64, (j // 64) // 32]) >> ((j // 64) % 32)) & 1)
+                 for (b, h, i, j) in inp.needles]
+    log(f"rows: {rows_ms:.3f} ms/step; stages {np.round(rst, 4).tolist()}; mean kept {kept_rows.mean():.2f}")
+    del rb, Or, bm, kv_rows, tt
+
     cold = None
     if not a.no_cold:
         # caches cold: a 1 GiB write (twice the 256 MB last-level cache) before each single step
@@ -352,6 +391,13 @@ def main():
                                           "attend_select": round(float(fst[3]), 4)},
                             "attend_select_TFLOPs": round(f_att / (fst[3] * 1e-3) / 1e12, 2),
                             "output_identical": same},
+        "row_selection": {"ms_per_step": round(rows_ms, 4),
+                          "stages_ms": {"meta_score_sigma_route": round(float(rst[0]), 4),
+                                        "select_rows": round(float(rst[1]), 4),
+                                        "attend_bitmap": round(float(rst[2]), 4)},
+                          "attend_bitmap_TFLOPs": round(f_rows / (rst[2] * 1e-3) / 1e12, 2),
+                          "mean_kept_blocks": round(float(kept_rows.mean()), 3),
+                          "needle_hit_rate": float(np.mean(rows_hits)) if rows_hits else None},
         "ms_per_step_median": round(float(np.median(step_ms)), 4),
         "cold": cold,
         "measured_peaks": probe,

@@ -21,6 +21,9 @@
  *   ugbs_score_select (Q, meta, workspace)   -> sigma (idx_sorted NULL)
  *   ugbs_route        (sigma, workspace)     -> trigger flags (kv_idx NULL)
  *   ugbs_attend_select(Q, K, V, workspace)   -> O
+ * or with per-row selection into tile bitmaps:
+ *   ugbs_select_rows  (Q, meta, trigger)     -> bitmap
+ *   ugbs_attend_bitmap(Q, K, V, bitmap)      -> O
  * No call synchronises the device; none allocates device memory.
  *
  * Diagnostics (Appendix D: sigma as a best-arm identification index), off
@@ -62,7 +65,7 @@ extern "C" {
 #define UGBS_API
 #endif
 
-#define UGBS_ABI_VERSION 5
+#define UGBS_ABI_VERSION 6
 #define UGBS_BLOCK 64          /* BLOCK_M = BLOCK_N = 64 tokens (Section 3.1, 3.2) */
 #define UGBS_MAX_BLOCKS 2048   /* N_B <= 2048, i.e. N <= 131072 */
 #define UGBS_MAX_KV_WIDTH 4096 /* kv_width accepted by ugbs_attend; rho * k_budget <= 4096 */
@@ -309,6 +312,34 @@ UGBS_API int ugbs_attend_select(const ugbs_problem* p, const void* Q, const void
                                 const float* scores, const uint8_t* trigger,
                                 const void* workspace, size_t workspace_bytes, void* O,
                                 void* stream);
+
+/* Per-row selection scattered into tile bitmaps (the per-row variant the
+ * Limitations of Section 4 name for the per-tile granularity of Section
+ * 3.2).  Every query row r of tile t ranks the candidates C(t) = {1..t-1}
+ * by its own score (A.2 before the max over rows: K-mean q_r . kbar_b,
+ * Quest sum_d max(q_rd kmax_bd, q_rd kmin_bd); bf16 products, fp32 sums)
+ * and keeps the forced blocks [0] or [0, t] and its R best candidates by
+ * (score descending, lower block first, -0 == +0), R = (trigger[b, t] ?
+ * rho k : k) - |F|, all of C(t) when it has at most R.  The tile's set is
+ * the union over its 64 rows.
+ *   Q, meta    : as for ugbs_score_select; may be NULL with row_scores.
+ *   row_scores : NULL, or [B, H, N, N_B] fp32 per-row scores that replace the
+ *                computed ones (entries of C(t) for the rows of tile t are read).
+ *   trigger    : [B, T] uint8 flags (nonzero = expanded), e.g. ugbs_route's;
+ *                all zero for plain per-row top-k.
+ *   bitmap     : [B, H, T, ceil(N_B / 32)] uint32, fully written: bit b % 32
+ *                of word b / 32 is set when block b is in the tile's set
+ *                (blocks after t never are). */
+UGBS_API int ugbs_select_rows(const ugbs_problem* p, const void* Q, const void* meta,
+                              const float* row_scores, const uint8_t* trigger, uint32_t* bitmap,
+                              void* stream);
+
+/* Stage 5 over tile bitmaps: as ugbs_attend with the set of blocks of tile
+ * (b, h, t) given by the set bits of bitmap[b, h, t, :] (bits of blocks
+ * after t are ignored).
+ *   bitmap : [B, H, T, ceil(N_B / 32)] uint32, 4-byte aligned. */
+UGBS_API int ugbs_attend_bitmap(const ugbs_problem* p, const void* Q, const void* K, const void* V,
+                                const uint32_t* bitmap, void* O, void* stream);
 
 /* Bytes of device workspace ugbs_score_select (without scores_in/scores_out),
  * ugbs_route and ugbs_attend_select need for problem p; one workspace

@@ -20,7 +20,7 @@ __all__ = [
     "KMEAN", "QUEST", "BLOCK", "Problem", "UGBSError", "lib", "library_path",
     "ugbs_block_meta", "ugbs_score_select", "ugbs_route", "ugbs_attend",
     "ugbs_workspace_bytes", "ugbs_status_string", "ugbs_abi_version",
-    "ugbs_attend_select", "prefill_fused",
+    "ugbs_attend_select", "prefill_fused", "ugbs_select_rows", "ugbs_attend_bitmap",
     "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads", "BAI_TILE_FIELDS", "BAI_HEAD_FIELDS",
     "bai_tile_records", "bai_head_records",
 ]
@@ -108,11 +108,14 @@ def lib():
         L.ugbs_status_string.restype = ctypes.c_char_p
         L.ugbs_abi_version.argtypes = []
         L.ugbs_attend_select.argtypes = [pp, P, P, P, P, P, P, ctypes.c_size_t, P, P]
+        L.ugbs_select_rows.argtypes = [pp, P, P, P, P, P, P]
+        L.ugbs_attend_bitmap.argtypes = [pp, P, P, P, P, P, P]
         L.ugbs_noise_scale.argtypes = [pp, P, P, P, P, P]
         L.ugbs_bai_tiles.argtypes = [pp, P, P, P, ctypes.c_int32, P, P]
         L.ugbs_bai_heads.argtypes = [pp, P, P, ctypes.c_int32, P, P]
         for f in ("ugbs_block_meta", "ugbs_score_select", "ugbs_route", "ugbs_attend", "ugbs_abi_version",
-                  "ugbs_attend_select", "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads"):
+                  "ugbs_attend_select", "ugbs_select_rows", "ugbs_attend_bitmap",
+                  "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -261,6 +264,38 @@ def ugbs_attend_select(p: Problem, Q, K, V, O, workspace=None, scores=None, trig
         nbytes = workspace.numel() * workspace.element_size()
     _raise("ugbs_attend_select", lib().ugbs_attend_select(ctypes.byref(p), q, k, v, sc, tr, ws, nbytes, o,
                                                           _stream(stream)))
+
+
+def bitmap_words(p: Problem) -> int:
+    return (p.NB + 31) // 32
+
+
+def ugbs_select_rows(p: Problem, trigger, bitmap, Q=None, meta=None, row_scores=None, stream=None):
+    """Per-row selection into tile bitmaps: bitmap [B,H,T,ceil(N_B/32)] int32
+    (uint32 words) from the per-row scores of Q against meta (or `row_scores`
+    [B,H,N,N_B] fp32) and the trigger flags [B,T] uint8."""
+    import torch
+    dev = bitmap.device
+    bf = _bf16()
+    tr = _check("trigger", trigger, (p.batch, p.T), (torch.uint8,), dev)
+    bm = _check("bitmap", bitmap, (p.batch, p.n_heads, p.T, bitmap_words(p)), (torch.int32,), dev)
+    q = _opt("Q", Q, (p.batch, p.n_heads, p.seq_len, p.head_dim), bf, dev)
+    m = _opt("meta", meta, (p.batch, p.n_kv_heads, p.NB, p.meta_width, p.head_dim), bf, dev)
+    rs = _opt("row_scores", row_scores, (p.batch, p.n_heads, p.seq_len, p.NB), (torch.float32,), dev)
+    _raise("ugbs_select_rows", lib().ugbs_select_rows(ctypes.byref(p), q, m, rs, tr, bm, _stream(stream)))
+
+
+def ugbs_attend_bitmap(p: Problem, Q, K, V, bitmap, O, stream=None):
+    """Stage 5 over the blocks set in bitmap [B,H,T,ceil(N_B/32)] (int32 words)."""
+    import torch
+    bf = _bf16()
+    dev = Q.device
+    q = _check("Q", Q, (p.batch, p.n_heads, p.seq_len, p.head_dim), bf)
+    k = _check("K", K, (p.batch, p.n_kv_heads, p.seq_len, p.head_dim), bf, dev)
+    v = _check("V", V, (p.batch, p.n_kv_heads, p.seq_len, p.head_dim), bf, dev)
+    bm = _check("bitmap", bitmap, (p.batch, p.n_heads, p.T, bitmap_words(p)), (torch.int32,), dev)
+    o = _check("O", O, (p.batch, p.n_heads, p.seq_len, p.head_dim), bf, dev)
+    _raise("ugbs_attend_bitmap", lib().ugbs_attend_bitmap(ctypes.byref(p), q, k, v, bm, o, _stream(stream)))
 
 
 # ---------------------------------------------------------------- diagnostics

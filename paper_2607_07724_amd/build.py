@@ -15,7 +15,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libugbs.so")
 ARCH = "gfx950"
 
-SOURCES = ["block_meta.hip", "score_select.hip", "route.hip", "attend.hip", "bai.hip", "abi.hip"]
+SOURCES = ["block_meta.hip", "score_select.hip", "route.hip", "attend.hip", "rowsel.hip", "bai.hip", "abi.hip"]
 
 CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

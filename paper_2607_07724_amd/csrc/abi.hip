@@ -152,6 +152,34 @@ int ugbs_attend_select(const ugbs_problem* p, const void* Q, const void* K, cons
       static_cast<uint16_t*>(O), static_cast<hipStream_t>(stream)));
 }
 
+int ugbs_select_rows(const ugbs_problem* p, const void* Q, const void* meta, const float* row_scores,
+                     const uint8_t* trigger, uint32_t* bitmap, void* stream) {
+  Shape s;
+  int st = make_shape(p, &s);
+  if (st) return st;
+  if (!trigger || !bitmap || (!row_scores && (!Q || !meta))) return UGBS_ERR_NULL;
+  if (!aligned(Q, 16) || !aligned(meta, 16) || !aligned(row_scores, 4) || !aligned(bitmap, 4))
+    return UGBS_ERR_ALIGN;
+  return hip_status(ugbs::launch_select_rows(s, static_cast<const uint16_t*>(Q),
+                                             static_cast<const uint16_t*>(meta), row_scores, trigger,
+                                             bitmap, static_cast<hipStream_t>(stream)));
+}
+
+int ugbs_attend_bitmap(const ugbs_problem* p, const void* Q, const void* K, const void* V,
+                       const uint32_t* bitmap, void* O, void* stream) {
+  Shape s;
+  int st = make_shape(p, &s);
+  if (st) return st;
+  if (!Q || !K || !V || !bitmap || !O) return UGBS_ERR_NULL;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) || !aligned(bitmap, 4))
+    return UGBS_ERR_ALIGN;
+  return hip_status(ugbs::launch_attend_bitmap(s, static_cast<const uint16_t*>(Q),
+                                               static_cast<const uint16_t*>(K),
+                                               static_cast<const uint16_t*>(V), bitmap,
+                                               static_cast<uint16_t*>(O),
+                                               static_cast<hipStream_t>(stream)));
+}
+
 int ugbs_noise_scale(const ugbs_problem* p, const void* Q, const void* meta, double* rough,
                      float* tau, void* stream) {
   Shape s;

@@ -59,7 +59,13 @@ struct AttnParams {
   const float* sel_scores;    // [B, H, T, N_B] tile scores, or nullptr: packed rows
   const float* sel_packed;    // packed candidate rows (workspace)
   const uint8_t* sel_trigger; // [B, T] trigger flags
+  // block bitmaps (ugbs_attend_bitmap)
+  const uint32_t* bitmap;     // [B, H, T, nw]
+  int nw;
 };
+
+// Where a tile's blocks come from.
+enum Mode { kLists = 0, kSelect = 1, kBitmap = 2 };
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -170,7 +176,7 @@ struct FetchPlan {
 template <int D>
 constexpr int kWavesPerEU = D > 128 ? 1 : 2;
 
-template <int D, bool SEL>
+template <int D, int MODE>
 __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(kWavesPerEU<D>, kWavesPerEU<D>)))
 attend_kernel(AttnParams P) {
   using L = Tile<D>;
@@ -211,7 +217,15 @@ attend_kernel(AttnParams P) {
     for (int i = lane; i < nwords; i += 64) s_bits[i] = 0u;
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_wave_barrier();
-    if constexpr (!SEL) {
+    if constexpr (MODE == kBitmap) {
+      // the caller's bitmap row; bits of blocks after t are dropped
+      const uint32_t* br = P.bitmap + rowid * P.nw;
+      for (int i = lane; i < nwords; i += 64) {
+        uint32_t v = br[i];
+        if (i == (u.t >> 5)) v &= (u.t & 31) == 31 ? 0xffffffffu : ((2u << (u.t & 31)) - 1u);
+        s_bits[i] = v;
+      }
+    } else if constexpr (MODE == kLists) {
       const int32_t* kr = P.kv_idx + rowid * P.kv_width;
       for (int base = 0; base < P.kv_width; base += 64) {
         const int sl = base + lane;
@@ -561,12 +575,12 @@ attend_kernel(AttnParams P) {
   }
 }
 
-// Workgroups of attend_kernel<D, SEL> resident at once on one XCD, for the given
+// Workgroups of attend_kernel<D, MODE> resident at once on one XCD, for the given
 // dynamic LDS size (occupancy per CU x CUs per XCD).  Cached per device as
 // one packed word (smem << 32 | value); a stale or missing entry only costs
 // a recomputation.  The value steers the visiting order, never the result.
 constexpr int kMaxDevices = 64;
-template <int D, bool SEL>
+template <int D, int MODE>
 int xcd_concurrency(size_t smem) {
   static std::atomic<uint64_t> cache[kMaxDevices];
   int dev = -1;
@@ -576,7 +590,7 @@ int xcd_concurrency(size_t smem) {
     if (e != 0 && (e >> 32) == (uint64_t)smem) return (int)(uint32_t)e;
   }
   int per_cu = 0, n_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attend_kernel<D, SEL>, 128, smem) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attend_kernel<D, MODE>, 128, smem) != hipSuccess)
     per_cu = 1;
   if (dev < 0 || hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) n_cu = 8;
   const int conc = per_cu * n_cu / 8 > 0 ? per_cu * n_cu / 8 : 1;
@@ -584,17 +598,17 @@ int xcd_concurrency(size_t smem) {
   return conc;
 }
 
-template <int D, bool SEL>
+template <int D, int MODE>
 hipError_t launch_t(AttnParams P, hipStream_t stream) {
   const size_t smem = sizeof(int32_t) * (size_t)P.kv_width;
   const int grid = ((P.n_units + 7) / 8) * 8;
   if (D > 128) {  // the K and V tiles alone take 64 KB of static LDS
-    const hipError_t e = hipFuncSetAttribute((const void*)attend_kernel<D, SEL>,
+    const hipError_t e = hipFuncSetAttribute((const void*)attend_kernel<D, MODE>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
   }
-  P.conc = xcd_concurrency<D, SEL>(smem);
-  attend_kernel<D, SEL><<<grid, 128, smem, stream>>>(P);
+  P.conc = xcd_concurrency<D, MODE>(smem);
+  attend_kernel<D, MODE><<<grid, 128, smem, stream>>>(P);
   return hipGetLastError();
 }
 
@@ -613,8 +627,8 @@ hipError_t launch_attend(const Shape& s, const uint16_t* Q, const uint16_t* K,
   P.kv_width = kv_width;
   P.n_units = s.B * s.H * s.T;
   P.scale_log2 = s.scale * 1.4426950408889634f;
-  if (s.d == 256) return launch_t<256, false>(P, stream);
-  return s.d == 128 ? launch_t<128, false>(P, stream) : launch_t<64, false>(P, stream);
+  if (s.d == 256) return launch_t<256, kLists>(P, stream);
+  return s.d == 128 ? launch_t<128, kLists>(P, stream) : launch_t<64, kLists>(P, stream);
 }
 
 hipError_t launch_attend_select(const Shape& s, const uint16_t* Q, const uint16_t* K,
@@ -634,8 +648,26 @@ hipError_t launch_attend_select(const Shape& s, const uint16_t* Q, const uint16_
   P.sel_scores = scores;
   P.sel_packed = ws ? reinterpret_cast<const float*>(ws + ws_scores_off(s)) : nullptr;
   P.sel_trigger = trigger ? trigger : ws + ws_trigger_off(s);
-  if (s.d == 256) return launch_t<256, true>(P, stream);
-  return s.d == 128 ? launch_t<128, true>(P, stream) : launch_t<64, true>(P, stream);
+  if (s.d == 256) return launch_t<256, kSelect>(P, stream);
+  return s.d == 128 ? launch_t<128, kSelect>(P, stream) : launch_t<64, kSelect>(P, stream);
+}
+
+hipError_t launch_attend_bitmap(const Shape& s, const uint16_t* Q, const uint16_t* K,
+                                const uint16_t* V, const uint32_t* bitmap, uint16_t* O,
+                                hipStream_t stream) {
+  AttnParams P{};
+  P.s = s;
+  P.Q = Q;
+  P.K = K;
+  P.V = V;
+  P.O = O;
+  P.kv_width = s.NB;  // a row may list every visible block
+  P.n_units = s.B * s.H * s.T;
+  P.scale_log2 = s.scale * 1.4426950408889634f;
+  P.bitmap = bitmap;
+  P.nw = (s.NB + 31) / 32;
+  if (s.d == 256) return launch_t<256, kBitmap>(P, stream);
+  return s.d == 128 ? launch_t<128, kBitmap>(P, stream) : launch_t<64, kBitmap>(P, stream);
 }
 
 }  // namespace ugbs

@@ -35,6 +35,13 @@ size_t score_scratch_bytes(const Shape& s);
 hipError_t launch_route(const Shape& s, int n_pop, int n_trig, const float* sigma,
                         const int32_t* idx_sorted, int32_t* kv_idx, float* sigma_bar,
                         float* tau, uint8_t* trigger, void* workspace, hipStream_t stream);
+// Per-row selection into tile bitmaps, and attention over bitmaps.
+hipError_t launch_select_rows(const Shape& s, const uint16_t* Q, const uint16_t* meta,
+                              const float* row_scores, const uint8_t* trigger, uint32_t* bitmap,
+                              hipStream_t stream);
+hipError_t launch_attend_bitmap(const Shape& s, const uint16_t* Q, const uint16_t* K,
+                                const uint16_t* V, const uint32_t* bitmap, uint16_t* O,
+                                hipStream_t stream);
 // Appendix D diagnostics.
 hipError_t launch_row_roughness(const Shape& s, const uint16_t* Q, const uint16_t* meta,
                                 double* rough, hipStream_t stream);

@@ -277,3 +277,30 @@ def test_rho_and_head_dim_256_accepted():
     p = good()
     p.rho = 0
     assert p.W == 2 * p.k_budget
+
+
+def test_row_selection_and_bitmap_attention_checks():
+    L = ugbs.lib()
+    p = good()
+    fake = ctypes.c_void_p(0x100000)
+    ERR_NULL, ERR_ALIGN = _enum("UGBS_ERR_NULL"), _enum("UGBS_ERR_ALIGN")
+    # select_rows: trigger and bitmap required; Q and meta unless row_scores
+    assert L.ugbs_select_rows(ctypes.byref(p), fake, fake, None, None, fake, None) == ERR_NULL
+    assert L.ugbs_select_rows(ctypes.byref(p), fake, fake, None, fake, None, None) == ERR_NULL
+    assert L.ugbs_select_rows(ctypes.byref(p), None, fake, None, fake, fake, None) == ERR_NULL
+    assert L.ugbs_select_rows(ctypes.byref(p), fake, None, None, fake, fake, None) == ERR_NULL
+    assert L.ugbs_select_rows(ctypes.byref(p), ctypes.c_void_p(0x100008), fake, None, fake, fake, None) == ERR_ALIGN
+    assert L.ugbs_select_rows(ctypes.byref(p), None, None, ctypes.c_void_p(0x100002), fake, fake,
+                              None) == ERR_ALIGN
+    assert L.ugbs_select_rows(ctypes.byref(p), fake, fake, None, fake, ctypes.c_void_p(0x100002),
+                              None) == ERR_ALIGN
+    for i in range(5):
+        args = [fake] * 5
+        args[i] = None
+        assert L.ugbs_attend_bitmap(ctypes.byref(p), *args, None) == ERR_NULL
+    assert L.ugbs_attend_bitmap(ctypes.byref(p), fake, fake, fake, ctypes.c_void_p(0x100002), fake,
+                                None) == ERR_ALIGN
+    bad = good(k_budget=2)
+    assert L.ugbs_select_rows(ctypes.byref(bad), fake, fake, None, fake, fake, None) == _enum("UGBS_ERR_BUDGET")
+    assert L.ugbs_attend_bitmap(ctypes.byref(good(head_dim=96)), fake, fake, fake, fake, fake,
+                                None) == _enum("UGBS_ERR_SHAPE")

@@ -1,0 +1,235 @@
+"""GPU parity of per-row selection into tile bitmaps (ugbs_select_rows) and
+attention over bitmaps (ugbs_attend_bitmap), against the per-row oracle.
+
+  - given the oracle's per-row scores: every bitmap word bit-exact (same
+    keys, same order, -0 == +0, ties by lower block), for both backbones,
+    d in {64, 128, 256}, rho in {1, 2, 3}, no / all / routed triggers;
+  - with the scores computed on the GPU (fp32 MFMA sums against the fp64
+    oracle): a block may differ only where, for some row of the tile, its
+    oracle score lies within 1e-3 (relative to the row's score spread) of
+    the row's last kept score;
+  - attention over a bitmap equals ugbs_attend over the same blocks bit for
+    bit and the fp64 oracle within max-abs 2e-2, RMS 2e-3;
+  - the layer (scores + sigma, route flags, per-row selection, attention)
+    against the oracle, rows with equal bitmaps compared within the bar.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_07724_amd as ugbs
+from paper_2607_07724_amd import synth
+
+from gpu_helpers import attention_error, dev, dev_bf16, host, host_bits
+
+pytestmark = pytest.mark.gpu
+ATOL_MAX, ATOL_RMS = 2e-2, 2e-3
+
+CASES = {
+    "C1": synth.WORKLOADS["C1"],
+    "kmean_d128_gqa4": synth.Workload("R1", 1, 8, 2, 128, 3072, 6, 0.25, synth.KMEAN, "offset",
+                                      needles=4, base_seed=61),
+    "quest_d64_b2": synth.Workload("R2", 2, 4, 2, 64, 2048, 5, 0.4, synth.QUEST, "mixture",
+                                   needles=4, needle_pairs=True, base_seed=62),
+    "kmean_d256_qknorm_rho3": synth.Workload("R3", 1, 4, 2, 256, 1536, 4, 0.3, synth.KMEAN, "offset",
+                                             qk_norm=True, rho=3, base_seed=63),
+    "quest_d256_rho1": synth.Workload("R4", 1, 2, 1, 256, 1024, 4, 0.5, synth.QUEST, "mixture",
+                                      rho=1, base_seed=64),
+}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need an MI355X; run them on the GPU box")
+    ugbs.lib()
+
+
+_cache = {}
+
+
+def case(name):
+    if name in _cache:
+        return _cache[name]
+    w = CASES[name]
+    inp = synth.generate(w, threads=8)
+    meta = oracle.block_meta(w.backbone, inp.K)
+    rows = oracle.row_scores(w.backbone, inp.Q, meta, w.Hkv)          # [B,H,T,64,T]
+    S = oracle.tile_scores(w.backbone, inp.Q, meta, w.Hkv)
+    idx, sig = oracle.select(S, w.k, rho=w.rho)
+    _, sb, tau, trig = oracle.route(sig, idx, w.k, w.q, rho=w.rho)
+    _cache[name] = dict(w=w, inp=inp, meta=meta, rows=rows, trig=trig, sb=sb, tau=tau)
+    return _cache[name]
+
+
+def problem(w, k=None, q=None):
+    return ugbs.Problem.make(w.B, w.H, w.Hkv, w.N, w.d, w.k if k is None else k,
+                             w.q if q is None else q, w.backbone, rho=w.rho)
+
+
+def flags(w, mode, c):
+    if mode == "route":
+        return c["trig"]
+    return np.full((w.B, w.T), 1 if mode == "all" else 0, np.uint8)
+
+
+def oracle_bits(c, w, k, trig):
+    units = oracle.all_units(w.B, w.H, w.T)
+    rows = c["rows"].reshape(-1, 64, w.T)
+    tu = np.array([trig[b, t] for b, h, t in units], np.uint8)
+    return oracle.select_rows(rows, units[:, 2], k, w.rho, tu).reshape(w.B, w.H, w.T, -1)
+
+
+def gpu_bits(p, c, w, trig, given_scores):
+    torch = __import__("torch")
+    bm = torch.full((w.B, w.H, w.T, ugbs.bitmap_words(p)), -1, dtype=torch.int32, device="cuda")
+    if given_scores:
+        # [B,H,T,64,T] -> [B,H,N,N_B]
+        rs = np.ascontiguousarray(c["rows"].reshape(w.B, w.H, w.T * 64, w.T))
+        ugbs.ugbs_select_rows(p, dev(trig), bm, row_scores=dev(rs))
+    else:
+        ugbs.ugbs_select_rows(p, dev(trig), bm, Q=dev_bf16(c["inp"].Q), meta=dev_bf16(c["meta"]))
+    torch.cuda.synchronize()
+    return host(bm).view(np.uint32)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+@pytest.mark.parametrize("mode", ["none", "all", "route"])
+def test_given_oracle_row_scores_bit_exact(name, mode):
+    c = case(name)
+    w = c["w"]
+    trig = flags(w, mode, c)
+    for k in sorted({3, w.k}):
+        p = problem(w, k=k)
+        assert np.array_equal(gpu_bits(p, c, w, trig, True), oracle_bits(c, w, k, trig)), (k, mode)
+
+
+def near_tie_bits_ok(gb, ob, rows, t, k_eff, rel=1e-3):
+    """Differing blocks must sit at some row's cut within rel of its spread."""
+    NB = rows.shape[-1]
+    diff = set(oracle.bitmap_blocks(gb, NB)) ^ set(oracle.bitmap_blocks(ob, NB))
+    if not diff:
+        return True, 0
+    nf = 1 if t == 0 else 2
+    R = min(k_eff - nf, max(t - 1, 0))
+    for blk in diff:
+        if blk == 0 or blk >= t:
+            return False, -1
+        ok = False
+        for r in range(64):
+            c = np.sort(rows[r, 1:t].astype(np.float64))[::-1]
+            cut, spread = c[R - 1], max(c[0] - c[-1], 1e-30)
+            if abs(float(rows[r, blk]) - cut) <= rel * max(spread, abs(cut)):
+                ok = True
+                break
+        if not ok:
+            return False, -1
+    return True, len(diff)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_computed_scores_against_oracle_up_to_near_ties(name):
+    c = case(name)
+    w = c["w"]
+    trig = c["trig"]
+    p = problem(w)
+    gb = gpu_bits(p, c, w, trig, False)
+    ob = oracle_bits(c, w, w.k, trig)
+    exempt = 0
+    for b in range(w.B):
+        for h in range(w.H):
+            for t in range(w.T):
+                k_eff = w.rho * w.k if trig[b, t] else w.k
+                ok, nd = near_tie_bits_ok(gb[b, h, t], ob[b, h, t], c["rows"][b, h, t], t, k_eff)
+                assert ok, (b, h, t)
+                exempt += nd > 0
+    assert exempt <= 0.02 * w.B * w.H * w.T
+
+
+def lists_from_bits(bits, NB):
+    B, H, T, _ = bits.shape
+    kv = np.full((B, H, T, NB), NB, np.int32)
+    for b in range(B):
+        for h in range(H):
+            for t in range(T):
+                lst = oracle.bitmap_blocks(bits[b, h, t], NB)
+                kv[b, h, t, :len(lst)] = lst
+    return kv
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_attend_bitmap_given_oracle_bitmap(name):
+    torch = __import__("torch")
+    c = case(name)
+    w, inp = c["w"], c["inp"]
+    p = problem(w)
+    ob = oracle_bits(c, w, w.k, c["trig"])
+    Q, K, V = dev_bf16(inp.Q), dev_bf16(inp.K), dev_bf16(inp.V)
+    O1, O2 = torch.empty_like(Q), torch.empty_like(Q)
+    ugbs.ugbs_attend_bitmap(p, Q, K, V, dev(ob.view(np.int32)), O1)
+    kv = lists_from_bits(ob, w.NB)
+    ugbs.ugbs_attend(p, Q, K, V, dev(kv), O2)
+    torch.cuda.synchronize()
+    a = host_bits(O1)
+    assert np.array_equal(a, host_bits(O2))
+    ref = oracle.attend(inp.Q, inp.K, inp.V, kv_idx=kv)
+    mx, rms = attention_error(a, ref)
+    assert mx <= ATOL_MAX and rms <= ATOL_RMS, (mx, rms)
+
+
+def test_bitmap_bits_after_the_tile_are_ignored():
+    torch = __import__("torch")
+    c = case("C1")
+    w, inp = c["w"], c["inp"]
+    p = problem(w)
+    ob = oracle_bits(c, w, w.k, c["trig"])
+    junk = ob.copy()
+    junk[..., 0] |= np.uint32(0xffff0000)                 # blocks 16..31 do not exist / are future
+    Q, K, V = dev_bf16(inp.Q), dev_bf16(inp.K), dev_bf16(inp.V)
+    O1, O2 = torch.empty_like(Q), torch.empty_like(Q)
+    ugbs.ugbs_attend_bitmap(p, Q, K, V, dev(ob.view(np.int32)), O1)
+    ugbs.ugbs_attend_bitmap(p, Q, K, V, dev(junk.view(np.int32)), O2)
+    torch.cuda.synchronize()
+    assert np.array_equal(host_bits(O1), host_bits(O2))
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_layer_with_row_selection(name):
+    torch = __import__("torch")
+    c = case(name)
+    w, inp = c["w"], c["inp"]
+    p = problem(w)
+    Q, K, V = dev_bf16(inp.Q), dev_bf16(inp.K), dev_bf16(inp.V)
+    bufs = ugbs.Buffers(p)
+    ugbs.ugbs_block_meta(p, K, bufs.meta)
+    ugbs.ugbs_score_select(p, Q, bufs.meta, None, bufs.sigma, workspace=bufs.workspace)
+    ugbs.ugbs_route(p, bufs.sigma, None, None, bufs.workspace, bufs.sigma_bar, bufs.tau, bufs.trigger)
+    bm = torch.empty((w.B, w.H, w.T, ugbs.bitmap_words(p)), dtype=torch.int32, device="cuda")
+    ugbs.ugbs_select_rows(p, bufs.trigger, bm, Q=Q, meta=bufs.meta)
+    O = torch.empty_like(Q)
+    ugbs.ugbs_attend_bitmap(p, Q, K, V, bm, O)
+    torch.cuda.synchronize()
+    gb = host(bm).view(np.uint32)
+    gtrig = host(bufs.trigger)
+    ob = oracle_bits(c, w, w.k, c["trig"])      # the oracle's own flags
+    ref = oracle.attend(inp.Q, inp.K, inp.V, kv_idx=lists_from_bits(ob, w.NB))
+    got = host_bits(O)
+    same = 0
+    for b in range(w.B):
+        for t in range(w.T):
+            if gtrig[b, t] != c["trig"][b, t]:        # a flip only next to the quantile
+                assert abs(float(c["sb"][b, t]) - float(c["tau"][b])) <= 1e-3, (b, t)
+        for h in range(w.H):
+            for t in range(w.T):
+                if gtrig[b, t] != c["trig"][b, t]:
+                    continue
+                k_eff = w.rho * w.k if gtrig[b, t] else w.k
+                ok, _ = near_tie_bits_ok(gb[b, h, t], ob[b, h, t], c["rows"][b, h, t], t, k_eff)
+                assert ok, (b, h, t)
+                if np.array_equal(gb[b, h, t], ob[b, h, t]):
+                    same += 1
+                    d = (got[b, h, 64 * t:64 * t + 64].astype(np.uint32) << 16).view(np.float32) - \
+                        ref[b, h, 64 * t:64 * t + 64]
+                    assert np.abs(d).max() <= ATOL_MAX
+    assert same >= 0.9 * w.B * w.H * w.T
