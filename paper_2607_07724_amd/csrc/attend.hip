@@ -1,7 +1,8 @@
 // Stage 5: block-sparse causal attention over kv_idx (A.10; Eq. (Attn)).
 //
-// One workgroup of two waves per (batch, query head, Q-tile) unit; wave w
-// owns query rows 32w..32w+31 of the tile.  The tile's kv_idx row is first
+// One workgroup per (batch, query head, Q-tile) unit: two waves of 32 query
+// rows (d <= 128) or four waves of 16 rows (d = 256); wave w owns rows
+// RPW w .. RPW w + RPW - 1 of the tile.  The tile's kv_idx row is first
 // turned into an ascending list of distinct blocks in 0..t (so the diagonal
 // block comes last), then the listed key blocks are visited one by one.
 //
@@ -12,7 +13,7 @@
 // d/8), of V at c ^ (2r mod d/8)), chosen so that the K-operand reads and the
 // transposing V reads below are free of LDS bank conflicts.  K and V have one
 // buffer each and are refilled in a split ping-pong: K(i+1) is fetched as
-// soon as both waves have finished S(i), V(i+1) as soon as both have
+// soon as all waves have finished S(i), V(i+1) as soon as all have
 // finished PV(i), so the fetches overlap the softmax and the other matrix
 // product.
 //
@@ -106,12 +107,22 @@ __device__ __forceinline__ float rows_max(float x) {
   return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
+// Waves per unit and 16-row tiles per wave: d <= 128 runs two waves of 32
+// query rows; d = 256 four waves of 16 rows (half the accumulators per wave,
+// so two waves still fit on a SIMD).
+template <int D>
+struct Geo {
+  static constexpr int RT = D > 128 ? 1 : 2;   // 16-row tiles per wave
+  static constexpr int NWV = 4 / RT;           // waves per unit (64 rows)
+  static constexpr int kThreads = 64 * NWV;
+};
+
 template <int D>
 struct Tile {
   static constexpr int CPR = D / 8;                 // 16-byte chunks per key row
   static constexpr int kElems = kBlock * D;         // one K or V block
   static constexpr int kLoads = kBlock * CPR / 64;  // direct loads per block (64 chunks each)
-  static constexpr int kLoadsPerWave = kLoads / 2;
+  static constexpr int kLoadsPerWave = kLoads / Geo<D>::NWV;
   static constexpr int kRowsPerLoad = 64 / CPR;
   // Element offset of 16-byte column c of row r.  K: column c ^ (r mod CPR),
   // so the 16 rows read by one K-operand load hit 16 different columns.
@@ -144,19 +155,24 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // rows inst*R .. inst*R+R-1 (R = kRowsPerLoad) into LDS bytes inst*1024 ..
 // +1023, lane l writing LDS chunk inst*64+l, which holds global chunk
 // (l mod CPR) ^ swizzle(row).  The swizzle depends on the load index only
-// through inst mod M, so each lane keeps M byte offsets (row within the load
-// and column), and the rows of the load are added to the wave-uniform base.
+// through inst mod M, so each lane keeps the byte offsets (row within the
+// load and column) of its wave's first min(M, loads per wave) loads, and
+// the rows of the load are added to the wave-uniform base.
 template <int D, bool V>
 struct FetchPlan {
   using L = Tile<D>;
   static constexpr int M = V ? (L::CPR > 2 * L::kRowsPerLoad ? L::CPR / (2 * L::kRowsPerLoad) : 1)
                              : (L::CPR > L::kRowsPerLoad ? L::CPR / L::kRowsPerLoad : 1);
-  static_assert(L::kLoadsPerWave % M == 0, "wave's first load must be a multiple of M");
-  uint32_t voff[M];
-  __device__ __forceinline__ void init(int lane) {
+  static constexpr int MW = M < L::kLoadsPerWave ? M : L::kLoadsPerWave;
+  // either the wave's loads wrap around the M offsets whole, or there are
+  // at most M of them
+  static_assert(L::kLoadsPerWave % M == 0 || L::kLoadsPerWave <= M, "load plan");
+  uint32_t voff[MW];
+  __device__ __forceinline__ void init(int lane, int w) {
 #pragma unroll
-    for (int m = 0; m < M; ++m) {
-      const int r = m * L::kRowsPerLoad + lane / L::CPR;
+    for (int m = 0; m < MW; ++m) {
+      const int inst = w * L::kLoadsPerWave + m;
+      const int r = inst * L::kRowsPerLoad + lane / L::CPR;
       const int c = (lane % L::CPR) ^ L::swz(r, V);
       voff[m] = (uint32_t)(((lane / L::CPR) * D + c * 8) * 2);
     }
@@ -165,24 +181,21 @@ struct FetchPlan {
 #pragma unroll
     for (int i = 0; i < L::kLoadsPerWave; ++i) {
       const int inst = w * L::kLoadsPerWave + i;
-      dma16(src_blk + (size_t)inst * L::kRowsPerLoad * D, voff[i % M], tile_lds + (uint32_t)(inst * 64 * 16));
+      dma16(src_blk + (size_t)inst * L::kRowsPerLoad * D, voff[i % MW], tile_lds + (uint32_t)(inst * 64 * 16));
     }
   }
 };
 
-// d <= 128: two waves per SIMD; d = 256 needs twice the accumulators and
-// query registers (O^T alone is 128 fp32 per lane), so one wave per SIMD
-// with the matrix accumulators in the AGPR half of the register file.
-template <int D>
-constexpr int kWavesPerEU = D > 128 ? 1 : 2;
-
+// Two waves per SIMD at every d (at d = 256 through the four-wave geometry).
 template <int D, int MODE>
-__global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(kWavesPerEU<D>, kWavesPerEU<D>)))
+__global__ void __launch_bounds__(Geo<D>::kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 attend_kernel(AttnParams P) {
   using L = Tile<D>;
   constexpr int KS = D / 32;      // k-steps of QK^T
   constexpr int DT = D / 16;      // 16-channel tiles of O^T
   constexpr int NW = L::kLoadsPerWave;
+  constexpr int RT = Geo<D>::RT;
+  constexpr int RPW = 16 * RT;    // query rows per wave
   __shared__ __align__(16) uint16_t s_k[L::kElems];
   __shared__ __align__(16) uint16_t s_v[L::kElems];
   extern __shared__ int32_t s_list[];          // [kv_width]: at most kv_width distinct blocks
@@ -356,16 +369,16 @@ attend_kernel(AttnParams P) {
 
   const size_t qo_base = ((size_t)u.b * s.H + u.h) * s.N + (size_t)u.t * kBlock;
   if (n == 0) {  // no attended key: O = 0
-    for (int i = tid; i < kBlock * D / 8; i += 128)
+    for (int i = tid; i < kBlock * D / 8; i += Geo<D>::kThreads)
       reinterpret_cast<uint4*>(P.O + qo_base * D)[i] = make_uint4(0, 0, 0, 0);
     return;
   }
 
   // ---- query rows as the B operand --------------------------------------
-  bf16x8 bq[2][KS];
+  bf16x8 bq[RT][KS];
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    const uint16_t* qr = P.Q + (qo_base + 32 * w + 16 * rt + c16) * D + 8 * g;
+  for (int rt = 0; rt < RT; ++rt) {
+    const uint16_t* qr = P.Q + (qo_base + RPW * w + 16 * rt + c16) * D + 8 * g;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) bq[rt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qr + 32 * ks));
   }
@@ -375,25 +388,29 @@ attend_kernel(AttnParams P) {
   const uint16_t* Vh = P.V + ((size_t)u.b * s.Hkv + kvh) * s.N * D;
   FetchPlan<D, false> kplan;
   FetchPlan<D, true> vplan;
-  kplan.init(lane);
-  vplan.init(lane);
+  kplan.init(lane, w);
+  vplan.init(lane, w);
   const uint32_t k_lds = __builtin_amdgcn_readfirstlane(lds_addr(s_k));
   const uint32_t v_lds = __builtin_amdgcn_readfirstlane(lds_addr(s_v));
 
-  f32x4 acc_o[DT][2];
+  f32x4 acc_o[DT][RT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt) acc_o[dt][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[2] = {-__builtin_huge_valf(), -__builtin_huge_valf()};
-  float l_run[2] = {0.f, 0.f};
+    for (int rt = 0; rt < RT; ++rt) acc_o[dt][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run[RT], l_run[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    m_run[rt] = -__builtin_huge_valf();
+    l_run[rt] = 0.f;
+  }
 
   // S^T = K Q^T : [64 keys x 32 rows] per wave, K from LDS
-  auto compute_s = [&](f32x4 (&sc)[4][2]) {
+  auto compute_s = [&](f32x4 (&sc)[4][RT]) {
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) sc[kt][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int rt = 0; rt < RT; ++rt) sc[kt][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
@@ -401,7 +418,7 @@ attend_kernel(AttnParams P) {
         const int r = 16 * kt + c16;
         const bf16x8 ak = as_bf16x8(*reinterpret_cast<const uint4*>(s_k + L::off(r, 4 * ks + g, false)));
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
+        for (int rt = 0; rt < RT; ++rt)
           sc[kt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, bq[rt][ks], sc[kt][rt], 0, 0, 0);
       }
     }
@@ -414,12 +431,12 @@ attend_kernel(AttnParams P) {
   int blk = listed(0);
   kplan.fetch(Kh + (size_t)blk * Tile<D>::kElems, k_lds, w);
   vplan.fetch(Vh + (size_t)blk * Tile<D>::kElems, v_lds, w);
-  f32x4 sc[4][2];
+  f32x4 sc[4][RT];
   wait_vmcnt<NW>();                      // K0 landed
   lds_barrier();
   compute_s(sc);
   wait_lgkm0();
-  lds_barrier();                         // both waves are done reading s_k
+  lds_barrier();                         // all waves are done reading s_k
   if (n > 1) kplan.fetch(Kh + (size_t)listed(1) * Tile<D>::kElems, k_lds, w);
 
   // One pipeline step for listed block `it`; MASK: it is the diagonal block
@@ -435,7 +452,7 @@ attend_kernel(AttnParams P) {
       lds_barrier();
     }
     // S(it+1): on the last block this re-reads s_k (no fetch is pending) and is discarded
-    f32x4 sn[4][2];
+    f32x4 sn[4][RT];
     __builtin_amdgcn_s_setprio(1);       // matrix-core phases issue ahead of other waves' fetch phases
     compute_s(sn);
 
@@ -444,8 +461,8 @@ attend_kernel(AttnParams P) {
     // exceeds it by more than 2^8, so p <= 256 and O is rescaled rarely.
     if constexpr (MASK) {
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
-        const int r = 32 * w + 16 * rt + c16;
+      for (int rt = 0; rt < RT; ++rt) {
+        const int r = RPW * w + 16 * rt + c16;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
@@ -453,11 +470,11 @@ attend_kernel(AttnParams P) {
             if ((16 * kt + 4 * g + i) > r) sc[kt][rt][i] = -__builtin_huge_valf();
       }
     }
-    float alpha[2];
-    uint32_t pb[2][2][4];
+    float alpha[RT];
+    uint32_t pb[RT][2][4];
     bool moved = false;
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
+    for (int rt = 0; rt < RT; ++rt) {
       float mx = fmaxf(fmaxf(sc[0][rt][0], sc[0][rt][1]), fmaxf(sc[0][rt][2], sc[0][rt][3]));
 #pragma unroll
       for (int kt = 1; kt < 4; ++kt)
@@ -486,22 +503,24 @@ attend_kernel(AttnParams P) {
         pb[rt][j][3] = pack_bf16(p[2 * j + 1][2], p[2 * j + 1][3]);
       }
     }
-    // interleave, in two halves: 8 K-operand reads, then one MFMA of
-    // S(it+1) per five softmax VALU instructions
+    // interleave, in two halves: the K-operand reads, then one MFMA of
+    // S(it+1) per few softmax VALU instructions (8 reads, 16 x (1 + 5) at
+    // d = 128)
+    constexpr int kHalfReads = 2 * KS, kHalfMfma = 2 * KS * RT, kVpm = RT == 2 ? 5 : 2;
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, kHalfReads, 0);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
+      for (int i = 0; i < kHalfMfma; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, kVpm, 0);
       }
     }
 
     __builtin_amdgcn_s_setprio(0);
     if (has_next) {
       wait_lgkm0();
-      lds_barrier();                     // both waves are done reading s_k
+      lds_barrier();                     // all waves are done reading s_k
       if (has_next2)
         kplan.fetch(Kh + (size_t)listed(it + 2) * Tile<D>::kElems, k_lds, w);
     }
@@ -515,7 +534,7 @@ attend_kernel(AttnParams P) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
+        for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
           for (int i = 0; i < 4; ++i) acc_o[dt][rt][i] *= alpha[rt];
     }
@@ -537,7 +556,7 @@ attend_kernel(AttnParams P) {
         const bf16x8 av = __builtin_bit_cast(
             bf16x8, (short __attribute__((ext_vector_type(8)))){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
+        for (int rt = 0; rt < RT; ++rt) {
           const bf16x8 bp = as_bf16x8(make_uint4(pb[rt][j][0], pb[rt][j][1], pb[rt][j][2], pb[rt][j][3]));
           acc_o[dt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bp, acc_o[dt][rt], 0, 0, 0);
         }
@@ -545,12 +564,12 @@ attend_kernel(AttnParams P) {
     }
     __builtin_amdgcn_s_setprio(0);
     wait_lgkm0();
-    lds_barrier();                       // both waves are done reading s_v
+    lds_barrier();                       // all waves are done reading s_v
     if (has_next) vplan.fetch(Vh + (size_t)nblk * Tile<D>::kElems, v_lds, w);
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) sc[kt][rt] = sn[kt][rt];
+      for (int rt = 0; rt < RT; ++rt) sc[kt][rt] = sn[kt][rt];
   };
 
   for (int it = 0; it + 1 < n; ++it) step(it, std::false_type{});
@@ -559,12 +578,12 @@ attend_kernel(AttnParams P) {
 
   // ---- normalise and store: lane holds O^T[16dt + 4g + i][row] ------------
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
+  for (int rt = 0; rt < RT; ++rt) {
     float l = l_run[rt];
     l += __shfl_xor(l, 16);
     l += __shfl_xor(l, 32);
     const float inv = (l > 0.f) ? 1.0f / l : 0.f;
-    const int r = 32 * w + 16 * rt + c16;
+    const int r = RPW * w + 16 * rt + c16;
     uint16_t* orow = P.O + (qo_base + r) * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
@@ -590,7 +609,8 @@ int xcd_concurrency(size_t smem) {
     if (e != 0 && (e >> 32) == (uint64_t)smem) return (int)(uint32_t)e;
   }
   int per_cu = 0, n_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attend_kernel<D, MODE>, 128, smem) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attend_kernel<D, MODE>, Geo<D>::kThreads, smem) !=
+      hipSuccess)
     per_cu = 1;
   if (dev < 0 || hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) n_cu = 8;
   const int conc = per_cu * n_cu / 8 > 0 ? per_cu * n_cu / 8 : 1;
@@ -608,7 +628,7 @@ hipError_t launch_t(AttnParams P, hipStream_t stream) {
     if (e != hipSuccess) return e;
   }
   P.conc = xcd_concurrency<D, MODE>(smem);
-  attend_kernel<D, MODE><<<grid, 128, smem, stream>>>(P);
+  attend_kernel<D, MODE><<<grid, Geo<D>::kThreads, smem, stream>>>(P);
   return hipGetLastError();
 }
 
