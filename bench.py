@@ -274,7 +274,7 @@ def main():
     att_ms = float(stage_avg[3])
     bytes_kv_gathered = 2.0 * float(kept.sum()) * 64 * w.d * 2
     roofline = {
-        "kernel": "attend_kernel<128>",
+        "kernel": f"attend_kernel<{w.d}, 0> (kv_idx lists)",
         "bound": "mfma",
         "achieved": round(f_att / (att_ms * 1e-3) / 1e12, 2),
         "peak": PEAK_BF16_TFLOPS,
