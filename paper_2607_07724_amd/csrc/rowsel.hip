@@ -6,14 +6,14 @@
 // (all of C(t) when fewer), and the tile attends to the union over its 64
 // rows, handed to the attention kernel as a bitmap of N_B bits.
 //
-// One workgroup (4 waves) per (b, h, t) unit, kv head by kv head, heaviest
+// One workgroup (8 waves) per (b, h, t) unit, kv head by kv head, heaviest
 // tile first.  The 64 rows go in four quarters of 16:
-//   scores     wave w computes the 16 x 16 score blocks of chunks w, w + 4,
+//   scores     wave w computes the 16 x 16 score blocks of chunks w, w + 8,
 //              ... on bf16 MFMA (the 16 query rows in registers as the A
 //              operand, the chunk's metadata rows straight from L2 as the B
 //              operand; Quest as the exact split [q- | q+] . [kmin; kmax],
 //              split per MFMA at d = 256) into an LDS array [16 rows x N_B];
-//   selection  wave w takes rows w, w + 4, w + 8, w + 12: keys, the top-3
+//   selection  wave w takes rows w and w + 8: keys, the top-3
 //              pre-filter and the radix threshold of the selection kernel,
 //              and an atomic OR of each kept block into the LDS bitmap.
 // The bitmap words of blocks 0..t are then stored (the rest zero).
@@ -22,7 +22,7 @@
 namespace ugbs {
 namespace {
 
-constexpr int kRowWaves = 4;
+constexpr int kRowWaves = 8;   // two per SIMD: the selection is latency-bound
 constexpr int kQuarter = 16;                 // query rows per pass
 constexpr int kRowSlots = UGBS_MAX_BLOCKS / 64;
 
@@ -156,38 +156,50 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
             a[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g));
           }
         }
-        for (int c = w; c < nchunks; c += kRowWaves) {
-          // block 1 + 16 c + c16; past the last candidate the lane reads block 1
-          const int p = 16 * c + c16;
+        // the B operands of the wave's next chunk are loaded while the current
+        // one is multiplied (metadata rows straight from L2)
+        constexpr int KB = FLY ? 2 * KS : KS;
+        auto load_b = [&](int c, uint4 (&bv)[KB]) {
+          const int p = 16 * c + c16;  // block 1 + p; past the last candidate block 1 is read
           const uint16_t* mrow = mhead + (size_t)(1 + (p < nc ? p : 0)) * KD + 8 * g;
+#pragma unroll
+          for (int j = 0; j < KB; ++j) {
+            const int off = FLY ? (j % KS) * 32 + (j / KS) * D : 32 * j;   // FLY: kmin k-steps, then kmax
+            bv[j] = *reinterpret_cast<const uint4*>(mrow + off);
+          }
+        };
+        uint4 cur[KB], nxt[KB];
+        if (w < nchunks) load_b(w, cur);
+        for (int c = w; c < nchunks; c += kRowWaves) {
+          if (c + kRowWaves < nchunks) load_b(c + kRowWaves, nxt);
+          const int p = 16 * c + c16;
           f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
           if constexpr (FLY) {
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-              const bf16x8 bmin = as_bf16x8(*reinterpret_cast<const uint4*>(mrow + 32 * ks));
-              const bf16x8 bmax = as_bf16x8(*reinterpret_cast<const uint4*>(mrow + D + 32 * ks));
               const uint4 raw = __builtin_bit_cast(uint4, a[ks]);
-              acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(neg_part(raw)), bmin, acc, 0, 0, 0);
-              acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(pos_part(raw)), bmax, acc, 0, 0, 0);
+              acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(neg_part(raw)), as_bf16x8(cur[ks]), acc, 0, 0, 0);
+              acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(pos_part(raw)), as_bf16x8(cur[KS + ks]), acc,
+                                                            0, 0, 0);
             }
           } else {
-            bf16x8 bv[KS];
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) bv[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(mrow + 32 * ks));
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks], bv[ks], acc, 0, 0, 0);
+            for (int ks = 0; ks < KS; ++ks)
+              acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks], as_bf16x8(cur[ks]), acc, 0, 0, 0);
           }
           // lane holds rows 4g + i of the quarter, block column c16
           if (p < nc) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) s_rows[(4 * g + i) * P.pitch + p] = acc[i];
           }
+#pragma unroll
+          for (int j = 0; j < KB; ++j) cur[j] = nxt[j];
         }
         __syncthreads();
         rows = s_rows;
         stride = (size_t)P.pitch;
       }
-      // ---- selection: wave w takes rows w, w + 4, w + 8, w + 12 ------------
+      // ---- selection: wave w takes rows w, w + 8 ----------------------------
       for (int r = w; r < kQuarter; r += kRowWaves)
         row_top(rows + (size_t)r * stride, nc, R, lane, s_bits, s_surv[w]);
       __syncthreads();  // s_rows is rewritten by the next quarter
