@@ -232,15 +232,12 @@ def main():
     rst = np.array([[revs[i][j].elapsed_time(revs[i][j + 1]) for j in range(3)] for i in range(a.steps)]).mean(axis=0)
     bmh = bm.cpu().numpy().view(np.uint32)
     kept_rows = np.unpackbits(bmh.view(np.uint8), axis=-1).reshape(w.B, w.H, w.T, -1).sum(axis=-1)
-    kv_rows = np.full((w.B, w.H, w.T, 1), w.NB, np.int32)   # flop count from the bitmaps' block sets
-    f_rows = 0.0
-    tt = np.arange(w.T)[None, None, :]
-    n_full = kept_rows - 1                                   # every set is [.., t]: t is the diagonal
-    f_rows = 4.0 * w.d * float(n_full.sum() * 64 * 64 + kept_rows.size * (64 * 65 // 2))
+    # attention flop from the bitmaps' block sets: every set holds its diagonal block t
+    f_rows = 4.0 * w.d * float((kept_rows - 1).sum() * 64 * 64 + kept_rows.size * (64 * 65 // 2))
     rows_hits = [int((int(bmh[b, h, i // 64, (j // 64) // 32]) >> ((j // 64) % 32)) & 1)
                  for (b, h, i, j) in inp.needles]
     log(f"rows: {rows_ms:.3f} ms/step; stages {np.round(rst, 4).tolist()}; mean kept {kept_rows.mean():.2f}")
-    del rb, Or, bm, kv_rows, tt
+    del rb, Or, bm
 
     cold = None
     if not a.no_cold:

@@ -233,3 +233,45 @@ def test_layer_with_row_selection(name):
                         ref[b, h, 64 * t:64 * t + 64]
                     assert np.abs(d).max() <= ATOL_MAX
     assert same >= 0.9 * w.B * w.H * w.T
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["C2", "C4"])
+def test_full_size_row_selection(name):
+    """32K / 128K in the benchmark's configuration: sampled tiles' bitmaps
+    against the per-row oracle (up to near-ties; flags from the oracle's own
+    route are not available at this size, so all tiles use plain top-k and
+    the routed flags path is covered above), and attention over the GPU's
+    bitmaps of sampled tiles against the fp64 oracle on the same blocks."""
+    torch = __import__("torch")
+    w = synth.WORKLOADS[name]
+    inp = synth.generate(w, threads=16)
+    p = problem(w)
+    Q, K, V = dev_bf16(inp.Q), dev_bf16(inp.K), dev_bf16(inp.V)
+    meta = torch.empty((w.B, w.Hkv, w.NB, p.meta_width, w.d), dtype=torch.bfloat16, device="cuda")
+    ugbs.ugbs_block_meta(p, K, meta)
+    trig = torch.zeros((w.B, w.T), dtype=torch.uint8, device="cuda")
+    bm = torch.empty((w.B, w.H, w.T, ugbs.bitmap_words(p)), dtype=torch.int32, device="cuda")
+    ugbs.ugbs_select_rows(p, trig, bm, Q=Q, meta=meta)
+    O = torch.empty_like(Q)
+    ugbs.ugbs_attend_bitmap(p, Q, K, V, bm, O)
+    torch.cuda.synchronize()
+    gb = host(bm).view(np.uint32)
+    g = np.random.default_rng(w.seed())
+    ts = sorted({2, w.k, w.k + 1, w.T - 1} | set(int(x) for x in g.integers(2, w.T, 6)))
+    units = np.array([(0, int(g.integers(0, w.H)), t) for t in ts], np.int32)
+    meta_np = oracle.block_meta(w.backbone, inp.K, nthreads=16)
+    rows = oracle.row_scores(w.backbone, inp.Q, meta_np, w.Hkv, units=units, nthreads=16)
+    ob = oracle.select_rows(rows, units[:, 2], w.k, w.rho, None)
+    for i, (b, h, t) in enumerate(units):
+        ok, _ = near_tie_bits_ok(gb[b, h, t], ob[i], rows[i], int(t), w.k)
+        assert ok, (b, h, t)
+    # attention of sampled tiles over the GPU's own block sets
+    kv = np.full((len(units), w.NB), w.NB, np.int32)
+    for i, (b, h, t) in enumerate(units):
+        lst = oracle.bitmap_blocks(gb[b, h, t], w.NB)
+        kv[i, :len(lst)] = lst
+    ref = oracle.attend(inp.Q, inp.K, inp.V, kv_idx=kv, units=units, nthreads=16)
+    got = np.stack([host_bits(O[b, h, 64 * t:64 * t + 64]) for b, h, t in units])
+    mx, rms = attention_error(got, ref)
+    assert mx <= ATOL_MAX and rms <= ATOL_RMS, (mx, rms)
