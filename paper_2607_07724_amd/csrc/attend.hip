@@ -206,9 +206,29 @@ attend_kernel(AttnParams P) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform per wave
   const int g = lane >> 4, c16 = lane & 15;
-  const int uid = xcd_remap(blockIdx.x, P.n_units);
-  if (uid >= P.n_units) return;
-  const Unit u = unit_of(uid, s);
+  // Work order: kv head by kv head across the whole device (all XCDs on one
+  // kv head's K/V at a time, so the memory-side cache holds the working
+  // set); within a kv head, XCD x takes tiles T-1-x, T-1-x-8, ... (heaviest
+  // first, every tile size on every XCD), the sibling query heads of a tile
+  // on one XCD one after another.  Workgroup j runs on XCD j mod 8.
+  Unit u;
+  {
+    const int n_x = blockIdx.x >> 3, x = blockIdx.x & 7;
+    const int tiles_x = s.T / 8;                       // tiles per XCD and kv head (T % 8 == 0)
+    const int hh = n_x / (tiles_x * s.G);
+    const int within = n_x - hh * tiles_x * s.G;
+    const int tr = 8 * (within / s.G) + x;
+    u.b = hh / s.Hkv;
+    u.h = (hh % s.Hkv) * s.G + within % s.G;
+    u.t = s.T - 1 - tr;
+    if (s.T % 8 != 0) {                                 // fall back: contiguous ranges per XCD
+      const int uid = xcd_remap(blockIdx.x, P.n_units);
+      if (uid >= P.n_units) return;
+      u = unit_of(uid, s);
+    } else if (hh >= s.B * s.Hkv) {
+      return;
+    }
+  }
   const int kvh = u.h / s.G;
   const size_t rowid = ((size_t)u.b * s.H + u.h) * s.T + u.t;
 
