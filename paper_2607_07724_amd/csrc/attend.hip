@@ -206,27 +206,32 @@ attend_kernel(AttnParams P) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform per wave
   const int g = lane >> 4, c16 = lane & 15;
-  // Work order: kv head by kv head across the whole device (all XCDs on one
-  // kv head's K/V at a time, so the memory-side cache holds the working
-  // set); within a kv head, XCD x takes tiles T-1-x, T-1-x-8, ... (heaviest
+  // Work order: two kv heads at a time across the whole device (XCDs 0-3 on
+  // one, 4-7 on the other, so the memory-side cache holds the working set),
+  // one kv head at a time when the (batch, kv head) count is odd; within a
+  // kv head the XCDs of its group take its tiles round-robin (heaviest
   // first, every tile size on every XCD), the sibling query heads of a tile
-  // on one XCD one after another.  Workgroup j runs on XCD j mod 8.
+  // one after another on the same XCD.  Workgroup j runs on XCD j mod 8.
   Unit u;
   {
+    const int nbh = s.B * s.Hkv;
+    const int hpp = (nbh % 2 == 0 && s.T % 4 == 0) ? 2 : 1;   // kv heads in flight
+    const int stride = 8 / hpp;                                // XCDs per kv head
     const int n_x = blockIdx.x >> 3, x = blockIdx.x & 7;
-    const int tiles_x = s.T / 8;                       // tiles per XCD and kv head (T % 8 == 0)
-    const int hh = n_x / (tiles_x * s.G);
-    const int within = n_x - hh * tiles_x * s.G;
-    const int tr = 8 * (within / s.G) + x;
-    u.b = hh / s.Hkv;
-    u.h = (hh % s.Hkv) * s.G + within % s.G;
-    u.t = s.T - 1 - tr;
-    if (s.T % 8 != 0) {                                 // fall back: contiguous ranges per XCD
+    if (s.T % stride != 0) {                                   // fall back: contiguous ranges per XCD
       const int uid = xcd_remap(blockIdx.x, P.n_units);
       if (uid >= P.n_units) return;
       u = unit_of(uid, s);
-    } else if (hh >= s.B * s.Hkv) {
-      return;
+    } else {
+      const int tiles_x = s.T / stride;                        // tiles per XCD and kv head
+      const int phase = n_x / (tiles_x * s.G);
+      const int within = n_x - phase * tiles_x * s.G;
+      const int hh = hpp * phase + x / stride;                 // (batch, kv head) index
+      if (hh >= nbh) return;
+      const int tr = stride * (within / s.G) + x % stride;
+      u.b = hh / s.Hkv;
+      u.h = (hh % s.Hkv) * s.G + within % s.G;
+      u.t = s.T - 1 - tr;
     }
   }
   const int kvh = u.h / s.G;
