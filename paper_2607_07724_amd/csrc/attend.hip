@@ -243,13 +243,15 @@ attend_kernel(AttnParams P) {
   // mask, is the last entry when present.
   //
   // Visiting order.  The j-th workgroup an XCD receives starts its walk at
-  // the first listed block >= (j mod conc) / conc of its key range and wraps
-  // around (the diagonal block stays last).  Workgroups follow each other on
-  // an XCD in the order of j, conc of them at a time, so the ones resident
-  // together sweep the key range in step and blocks they share stay in that
-  // XCD's L2.  The order changes only the summation order of the softmax.
+  // the first listed block >= (j mod 2 conc) / (2 conc) of its key range and
+  // wraps around (the diagonal block stays last).  Workgroups follow each
+  // other on an XCD in the order of j, conc of them at a time, so the ones
+  // resident together sweep the key range in step and blocks they share
+  // stay in that XCD's L2 (a period of 2 conc measured best, 1 and 4 conc
+  // slower).  The order changes only the summation order of the softmax.
   const int j_xcd = blockIdx.x >> 3;
-  const int start_blk = (int)(((long long)(j_xcd % P.conc) * u.t) / P.conc);
+  const int period = 2 * P.conc;
+  const int start_blk = (int)(((long long)(j_xcd % period) * u.t) / period);
   if (w == 0) {
     const int nwords = (u.t >> 5) + 1;                 // bitmap words covering blocks 0..t
     for (int i = lane; i < nwords; i += 64) s_bits[i] = 0u;
