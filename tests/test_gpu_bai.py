@@ -46,7 +46,7 @@ N_S = 64
 def _need_gpu():
     torch = pytest.importorskip("torch")
     if not torch.cuda.is_available():
-        pytest.fail("GPU tests need an MI355X; run them on the GPU box")
+        pytest.fail("GPU tests need an MI355X (gfx950) visible to torch")
     ugbs.lib()
 
 

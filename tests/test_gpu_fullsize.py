@@ -33,7 +33,7 @@ BLK = 64
 def _need_gpu():
     torch = pytest.importorskip("torch")
     if not torch.cuda.is_available():
-        pytest.fail("GPU tests need an MI355X; run them on the GPU box")
+        pytest.fail("GPU tests need an MI355X (gfx950) visible to torch")
     ugbs.lib()
 
 

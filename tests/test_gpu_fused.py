@@ -40,7 +40,7 @@ CASES = {
 def _need_gpu():
     torch = pytest.importorskip("torch")
     if not torch.cuda.is_available():
-        pytest.fail("GPU tests need an MI355X; run them on the GPU box")
+        pytest.fail("GPU tests need an MI355X (gfx950) visible to torch")
     ugbs.lib()
 
 
