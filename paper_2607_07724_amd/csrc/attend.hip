@@ -247,10 +247,13 @@ attend_kernel(AttnParams P) {
   // wraps around (the diagonal block stays last).  Workgroups follow each
   // other on an XCD in the order of j, conc of them at a time, so the ones
   // resident together sweep the key range in step and blocks they share
-  // stay in that XCD's L2 (a period of 2 conc measured best, 1 and 4 conc
-  // slower).  The order changes only the summation order of the softmax.
+  // stay in that XCD's L2.  Measured at 128K: with kv_idx lists (about 70
+  // blocks per tile, or every visible block) a period of 2 conc is best (1
+  // and 4 conc slower); with the per-row bitmaps (hundreds of blocks per
+  // tile) 1 conc is 9% faster than 2 conc.  The order changes only the
+  // summation order of the softmax.
   const int j_xcd = blockIdx.x >> 3;
-  const int period = 2 * P.conc;
+  const int period = (MODE == kBitmap ? 1 : 2) * P.conc;
   const int start_blk = (int)(((long long)(j_xcd % period) * u.t) / period);
   if (w == 0) {
     const int nwords = (u.t >> 5) + 1;                 // bitmap words covering blocks 0..t

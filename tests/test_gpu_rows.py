@@ -171,11 +171,12 @@ def test_attend_bitmap_given_oracle_bitmap(name):
     kv = lists_from_bits(ob, w.NB)
     ugbs.ugbs_attend(p, Q, K, V, dev(kv), O2)
     torch.cuda.synchronize()
-    a = host_bits(O1)
-    assert np.array_equal(a, host_bits(O2))
+    # both walk the same blocks; the kernels start their walks at different
+    # points (their own visiting orders), so they agree up to rounding
     ref = oracle.attend(inp.Q, inp.K, inp.V, kv_idx=kv)
-    mx, rms = attention_error(a, ref)
-    assert mx <= ATOL_MAX and rms <= ATOL_RMS, (mx, rms)
+    for got in (host_bits(O1), host_bits(O2)):
+        mx, rms = attention_error(got, ref)
+        assert mx <= ATOL_MAX and rms <= ATOL_RMS, (mx, rms)
 
 
 def test_bitmap_bits_after_the_tile_are_ignored():
