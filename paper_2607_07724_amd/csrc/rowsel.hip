@@ -6,25 +6,28 @@
 // (all of C(t) when fewer), and the tile attends to the union over its 64
 // rows, handed to the attention kernel as a bitmap of N_B bits.
 //
-// One workgroup (8 waves) per (b, h, t) unit, kv head by kv head, heaviest
+// One workgroup (16 waves) per (b, h, t) unit, kv head by kv head, heaviest
 // tile first.  The 64 rows go in four quarters of 16:
-//   scores     wave w computes the 16 x 16 score blocks of chunks w, w + 8,
+//   scores     wave w computes the 16 x 16 score blocks of chunks w, w + 16,
 //              ... on bf16 MFMA (the 16 query rows in registers as the A
 //              operand, the chunk's metadata rows straight from L2 as the B
 //              operand; Quest as the exact split [q- | q+] . [kmin; kmax],
 //              split per MFMA at d = 256) into an LDS array [16 rows x N_B];
-//   selection  wave w takes rows w and w + 8: keys, the top-3
-//              pre-filter and the radix threshold of the selection kernel,
-//              and an atomic OR of each kept block into the LDS bitmap.
+//   selection  wave w takes row w: keys, the top-3 pre-filter and the radix
+//              threshold of the selection kernel (the survivors staged in
+//              the row's own LDS space once its keys are in registers), and
+//              an atomic OR of each kept block into the LDS bitmap.
 // The bitmap words of blocks 0..t are then stored (the rest zero).
 #include "select_common.h"
 
 namespace ugbs {
 namespace {
 
-constexpr int kRowWaves = 8;   // two per SIMD: the selection is latency-bound
+constexpr int kRowWaves = 16;  // four per SIMD, one row each: the selection is latency-bound
 constexpr int kQuarter = 16;                 // query rows per pass
 constexpr int kRowSlots = UGBS_MAX_BLOCKS / 64;
+constexpr int kSurvivors = 256;               // pre-filter survivors per row
+constexpr int kMinPitch = 2 * kSurvivors;     // floats: a row's LDS region holds its survivors
 
 struct RowParams {
   Shape s;
@@ -34,7 +37,7 @@ struct RowParams {
   const uint8_t* trigger;   // [B, T] trigger flags
   uint32_t* bitmap;         // [B, H, T, nw]
   int nw;
-  int pitch;                // floats per LDS score row
+  int pitch;                // floats per LDS score row (>= kMinPitch)
 };
 
 // The R best keys of one row (positions 0..nc-1 = blocks 1..nc) set in bits.
@@ -61,7 +64,8 @@ __device__ __forceinline__ void row_top(const float* row, int nc, int R, int lan
     }
     bool exact0;
     const uint32_t t0 = kth_largest<3>(top3, 3, R, &exact0);
-    constexpr int kSurv = 256;
+    constexpr int kSurv = kSurvivors;
+    wave_lds_sync();  // the row's keys are in registers: s_surv may reuse its space
     const uint64_t ltm = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     int ns = 0;
 #pragma unroll
@@ -104,9 +108,10 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
   constexpr int KD = QUEST ? 2 * D : D;        // metadata row length
   constexpr bool FLY = QUEST && D >= 256;      // split per MFMA (register budget)
   constexpr int KS = FLY ? D / 32 : KD / 32;   // A registers per lane
-  extern __shared__ __align__(16) float s_rows[];     // [16][pitch]
+  // [16][pitch]: the quarter's scores; row r's region then holds the
+  // survivors of row r (also when the scores come from memory)
+  extern __shared__ __align__(16) float s_rows[];
   __shared__ uint32_t s_bits[UGBS_MAX_BLOCKS / 32];
-  __shared__ uint64_t s_surv[kRowWaves][256];
   const Shape& s = P.s;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -156,8 +161,7 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
             a[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g));
           }
         }
-        // the B operands of the wave's next chunk are loaded while the current
-        // one is multiplied (metadata rows straight from L2)
+        // the chunk's metadata rows straight from L2 as the B operand
         constexpr int KB = FLY ? 2 * KS : KS;
         auto load_b = [&](int c, uint4 (&bv)[KB]) {
           const int p = 16 * c + c16;  // block 1 + p; past the last candidate block 1 is read
@@ -168,10 +172,9 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
             bv[j] = *reinterpret_cast<const uint4*>(mrow + off);
           }
         };
-        uint4 cur[KB], nxt[KB];
-        if (w < nchunks) load_b(w, cur);
         for (int c = w; c < nchunks; c += kRowWaves) {
-          if (c + kRowWaves < nchunks) load_b(c + kRowWaves, nxt);
+          uint4 cur[KB];
+          load_b(c, cur);
           const int p = 16 * c + c16;
           f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
           if constexpr (FLY) {
@@ -192,16 +195,15 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) s_rows[(4 * g + i) * P.pitch + p] = acc[i];
           }
-#pragma unroll
-          for (int j = 0; j < KB; ++j) cur[j] = nxt[j];
         }
         __syncthreads();
         rows = s_rows;
         stride = (size_t)P.pitch;
       }
-      // ---- selection: wave w takes rows w, w + 8 ----------------------------
+      // ---- selection: wave w takes row w ------------------------------------
       for (int r = w; r < kQuarter; r += kRowWaves)
-        row_top(rows + (size_t)r * stride, nc, R, lane, s_bits, s_surv[w]);
+        row_top(rows + (size_t)r * stride, nc, R, lane, s_bits,
+                reinterpret_cast<uint64_t*>(s_rows + (size_t)r * P.pitch));
       __syncthreads();  // s_rows is rewritten by the next quarter
     }
   }
@@ -212,8 +214,8 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
 
 template <int D, bool QUEST>
 hipError_t launch_rows(RowParams P, hipStream_t stream) {
-  const size_t smem = P.row_scores ? 0 : sizeof(float) * (size_t)kQuarter * P.pitch;
-  if (smem + sizeof(uint32_t) * (UGBS_MAX_BLOCKS / 32) + 8 * kRowWaves * 256 > 65536) {
+  const size_t smem = sizeof(float) * (size_t)kQuarter * P.pitch;
+  if (smem + sizeof(uint32_t) * (UGBS_MAX_BLOCKS / 32) > 65536) {
     const hipError_t e = hipFuncSetAttribute((const void*)rowsel_kernel<D, QUEST>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
@@ -237,7 +239,9 @@ hipError_t launch_select_rows(const Shape& s, const uint16_t* Q, const uint16_t*
   P.trigger = trigger;
   P.bitmap = bitmap;
   P.nw = (s.NB + 31) / 32;
-  P.pitch = ((s.NB + 3) & ~3) + 4;  // padded against bank conflicts of the column writes
+  // padded against bank conflicts of the column writes; with scores from
+  // memory the rows only hold survivors
+  P.pitch = row_scores ? kMinPitch : std::max(((s.NB + 3) & ~3) + 4, kMinPitch);
   const bool quest = s.backbone == UGBS_QUEST;
   if (s.d == 256) return quest ? launch_rows<256, true>(P, stream) : launch_rows<256, false>(P, stream);
   if (s.d == 128) return quest ? launch_rows<128, true>(P, stream) : launch_rows<128, false>(P, stream);
