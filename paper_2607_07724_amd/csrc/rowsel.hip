@@ -41,8 +41,13 @@ struct RowParams {
 };
 
 // The R best keys of one row (positions 0..nc-1 = blocks 1..nc) set in bits.
-__device__ __forceinline__ void row_top(const float* row, int nc, int R, int lane, uint32_t* bits,
+__device__ __forceinline__ void row_top(const float* row, int nc, int R, int lane_in, uint32_t* bits,
                                         uint64_t* s_surv) {
+  // the lane index passes through an opaque move, so the per-slot values
+  // derived from it are recomputed per row instead of being hoisted out of
+  // the row loop (and spilled: 16 waves leave 128 registers per lane)
+  int lane;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(lane) : "v"(lane_in));
   const int nslots = (nc + 63) / 64;
   uint32_t keys[kRowSlots];
 #pragma unroll
