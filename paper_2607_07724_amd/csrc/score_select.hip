@@ -18,9 +18,9 @@
 // the 16-byte column c of row r sits at c ^ (r mod 16), which makes the
 // operand reads bank-conflict free.  The max over the tile's rows (A.3) is
 // the max over a lane's 16 accumulators and then across the four 16-lane
-// groups; the row of tile scores collects in LDS and goes to memory once,
-// into the caller's [.., N_B] score tensor or into packed rows of the
-// workspace (row (b, h, t) holds the t-1 candidates 1..t-1).
+// groups; each chunk's 16 tile scores go straight to memory, into the
+// caller's [.., N_B] score tensor or into packed rows of the workspace (row
+// (b, h, t) holds the t-1 candidates 1..t-1).
 //
 // select_kernel: one wave per unit, heaviest tile first.  Tile scores
 // become order-preserving 32-bit keys (-0 folded into +0).  A per-lane
@@ -59,7 +59,6 @@ struct SelParams {
   int n_wg;       // score-kernel workgroups
   int wave_lds;   // bytes of per-wave LDS of the selection kernel (survivors)
   int ring_lds;   // bytes of the metadata ring
-  int row_lds;    // bytes of per-wave LDS of the score kernel (one row of scores)
 };
 
 // max over the four 16-lane rows (lanes l, l^16, l^32, l^48) with the gfx950
@@ -204,10 +203,6 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
   const int nc = (t >= 1) ? t - 1 : 0;
 
   unsigned char* ring = smem;
-  // this wave's tile scores stay in LDS until the chunk loop is done, so the
-  // only vector-memory operations in flight there are the ring's loads (the
-  // loop's vmcnt waits count nothing else)
-  float* s_row = reinterpret_cast<float*>(smem + P.ring_lds + w * P.row_lds);
 
   // this unit's candidate scores 1..nc: packed rows, or the full [.., N_B] row
   float* dst = PACKED ? P.scratch + packed_row(gr.b * s.H + h, t, s.T)
@@ -321,14 +316,13 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) mx = fmaxf(mx, acc[rt][i]);
           mx = wave_max16(mx);
-          if (g == 0 && pos < nc) s_row[pos] = mx;
+          // straight to memory: a 64-byte store per chunk.  The loop's vmcnt
+          // waits still count ring loads correctly: loads complete in issue
+          // order, so while a chunk is pending every later ring load is too,
+          // and an earlier store in flight can only lengthen a wait
+          if (g == 0 && pos < nc) dst[pos] = mx;
         }
       }
-    }
-    if (active && !ROUGH) {
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      __builtin_amdgcn_wave_barrier();
-      for (int p = lane; p < nc; p += 64) dst[p] = s_row[p];
     }
   }
   if constexpr (ROUGH) {
@@ -537,8 +531,7 @@ template <int D, bool QUEST, int OUT>
 hipError_t launch_score(SelParams P, hipStream_t stream) {
   using MC = MetaChunk<D, QUEST>;
   P.ring_lds = kRing * MC::kBytes;
-  P.row_lds = OUT == kOutRough ? 0 : (P.s.NB * 4 + 15) & ~15;
-  const size_t smem = (size_t)P.ring_lds + (size_t)P.GW * P.row_lds;
+  const size_t smem = (size_t)P.ring_lds;
   if (smem > 65536) {
     const hipError_t e = hipFuncSetAttribute((const void*)score_kernel<D, QUEST, OUT>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
@@ -613,7 +606,6 @@ hipError_t launch_score_select(const Shape& s, const uint16_t* Q, const uint16_t
   if (sel_bytes < 8 * kSurvivors) sel_bytes = 8 * kSurvivors;
   P.wave_lds = sel_bytes;
   P.ring_lds = 0;
-  P.row_lds = 0;
   if (scores_in) return launch_select<false>(P, stream);
   if (scores_out) {
     const hipError_t e = launch_score_d<kOutFull>(P, stream);
