@@ -12,7 +12,7 @@
 // so Qx = [q- | q+] and Mx = [kmin | kmax] (KD = 2d, the metadata row as
 // stored).  Every product is an exact bf16 x bf16 product; sums are fp32.
 // The wave's 64-row Qx tile stays in registers as the A operand.  Metadata
-// rows (the B operand) come in chunks of 16 blocks that the workgroup's
+// rows (the B operand) come in chunks of 16 or 32 blocks that the workgroup's
 // waves fetch together with direct-to-LDS loads into a 4-slot ring (three
 // chunks in flight), so each chunk crosses L2 once per sibling group; in LDS
 // the 16-byte column c of row r sits at c ^ (r mod 16), which makes the
@@ -40,7 +40,6 @@ namespace {
 constexpr int kMaxGroup = 4;    // sibling query heads per workgroup
 constexpr int kSelWaves = 4;    // units (waves) per selection workgroup
 constexpr int kRing = 4;        // metadata chunk slots (kRing - 1 in flight)
-constexpr int kChunk = 16;      // blocks per metadata chunk
 
 #define LDS_AS __attribute__((address_space(3)))
 
@@ -119,12 +118,17 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const LDS_AS void*)p;
 }
 
+// Blocks per metadata chunk: 32 (two 16-block MFMA column tiles per
+// barrier) where the query tile already holds the kernel at two waves per
+// SIMD (Quest d 128, K-mean d 256), 16 where the second accumulator set
+// would cost a wave (measured: 4-7% faster, 3-4% slower respectively).
 template <int D, bool QUEST>
 struct MetaChunk {
+  static constexpr int kBlocks = ((QUEST && D == 128) || (!QUEST && D == 256)) ? 32 : 16;
   static constexpr int KD = QUEST ? 2 * D : D;
   static constexpr int CPR = KD / 8;                   // 16-byte columns per metadata row
   static constexpr int SWZ = (CPR < 16 ? CPR : 16) - 1;
-  static constexpr int kBytes = kChunk * KD * 2;
+  static constexpr int kBytes = kBlocks * KD * 2;
   static constexpr int kLoads = kBytes / 1024;         // 1 KiB direct loads per chunk
   __device__ static __forceinline__ int off(int r, int c) { return (r * CPR + (c ^ (r & SWZ))) * 16; }
 };
@@ -237,34 +241,28 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
     // ---- metadata ring: chunk c holds candidate blocks 1 + 16c .. 16c + 16
     const uint16_t* mhead = P.meta + ((size_t)gr.b * s.Hkv + gr.kvh) * s.NB * KD;
     const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(ring));
-    const int nchunks = (nc + kChunk - 1) / kChunk;
+    const int nchunks = (nc + MC::kBlocks - 1) / MC::kBlocks;
     // this wave issues the chunk's 1 KiB loads i = w, w + GW, ...
     const int n_mine = (MC::kLoads - w + P.GW - 1) / P.GW;
-    // this wave's share of a chunk: loads i = w, w + GW, ... (at most 8);
-    // lane offsets within the chunk are fixed, only the base moves
+    // this wave's share of a chunk: loads i = w, w + GW, ...; the lane
+    // offsets within the chunk are recomputed per issue (a few integer
+    // operations), only the base moves
     constexpr int kMaxMine = MC::kLoads;
-    uint32_t voff[kMaxMine], vrow[kMaxMine];
-#pragma unroll
-    for (int j = 0; j < kMaxMine; ++j) {
-      const int i = w + j * P.GW;
-      const int p = i * 64 + lane;                    // 16-byte LDS chunk of the slot
-      const int r = p / MC::CPR;                      // block row within the chunk
-      const int col = (p % MC::CPR) ^ (r & MC::SWZ);
-      vrow[j] = (uint32_t)r;
-      voff[j] = (uint32_t)((r * KD + col * 8) * 2);
-    }
     auto issue = [&](int c) {
       const uint32_t slot = ring_lds + (uint32_t)((c % kRing) * MC::kBytes);
-      const uint16_t* base = mhead + (size_t)__builtin_amdgcn_readfirstlane(1 + kChunk * c) * KD;
-      const bool last = kChunk * (c + 1) >= nc;       // wave-uniform
+      const uint16_t* base = mhead + (size_t)__builtin_amdgcn_readfirstlane(1 + MC::kBlocks * c) * KD;
+      const bool last = MC::kBlocks * (c + 1) >= nc;       // wave-uniform
 #pragma unroll
       for (int j = 0; j < kMaxMine; ++j) {
         const int i = w + j * P.GW;
         if (i < MC::kLoads) {
+          const int p = i * 64 + lane;                  // 16-byte LDS chunk of the slot
+          const int r = p / MC::CPR;                    // block row within the chunk
+          const int col = (p % MC::CPR) ^ (r & MC::SWZ);
           // rows past the last candidate re-read the chunk's first row, which
-          // is a candidate (1 + 16c <= nc for every issued chunk)
-          uint32_t off = voff[j];
-          if (last && 1 + kChunk * c + (int)vrow[j] > nc) off -= vrow[j] * (uint32_t)(KD * 2);
+          // is a candidate (1 + kBlocks c <= nc for every issued chunk)
+          const int rr = (last && 1 + MC::kBlocks * c + r > nc) ? 0 : r;
+          const uint32_t off = (uint32_t)((rr * KD + col * 8) * 2);
           dma16(base, off, __builtin_amdgcn_readfirstlane(slot + i * 1024));
         }
       }
@@ -279,48 +277,52 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
       if (c + kRing - 1 < nchunks) issue(c + kRing - 1);
       if (active) {
         const unsigned char* slot = ring + (c % kRing) * MC::kBytes;
-        f32x4 acc[4];
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if constexpr (FLY) {
-          // min(q,0) . kmin + max(q,0) . kmax, k-step by k-step
+        for (int ct = 0; ct < MC::kBlocks / 16; ++ct) {   // 16-block column tiles of the chunk
+          const int br = 16 * ct + c16;                  // block row of this lane's column
+          f32x4 acc[4];
 #pragma unroll
-          for (int ks = 0; ks < KA; ++ks) {
-            const bf16x8 bmin = as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(c16, 4 * ks + g)));
-            const bf16x8 bmax =
-                as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(c16, 4 * (ks + D / 32) + g)));
+          for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+          if constexpr (FLY) {
+            // min(q,0) . kmin + max(q,0) . kmax, k-step by k-step
 #pragma unroll
-            for (int rt = 0; rt < 4; ++rt) {
-              const uint4 raw = __builtin_bit_cast(uint4, a[rt][ks]);
-              acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(neg_part(raw)), bmin, acc[rt], 0, 0, 0);
-              acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(pos_part(raw)), bmax, acc[rt], 0, 0, 0);
+            for (int ks = 0; ks < KA; ++ks) {
+              const bf16x8 bmin = as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(br, 4 * ks + g)));
+              const bf16x8 bmax =
+                  as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(br, 4 * (ks + D / 32) + g)));
+#pragma unroll
+              for (int rt = 0; rt < 4; ++rt) {
+                const uint4 raw = __builtin_bit_cast(uint4, a[rt][ks]);
+                acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(neg_part(raw)), bmin, acc[rt], 0, 0, 0);
+                acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(pos_part(raw)), bmax, acc[rt], 0, 0, 0);
+              }
+            }
+          } else {
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+              const bf16x8 b = as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(br, 4 * ks + g)));
+#pragma unroll
+              for (int rt = 0; rt < 4; ++rt)
+                acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][ks], b, acc[rt], 0, 0, 0);
             }
           }
-        } else {
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks) {
-            const bf16x8 b = as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(c16, 4 * ks + g)));
+          const int pos = MC::kBlocks * c + br;
+          if constexpr (ROUGH) {
+            const float sq = row_diff_sq(acc, lane);
+            rough += (pos < nc) ? (double)sq : 0.0;
+          } else {
+            float mx = acc[0][0];
 #pragma unroll
             for (int rt = 0; rt < 4; ++rt)
-              acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][ks], b, acc[rt], 0, 0, 0);
+#pragma unroll
+              for (int i = 0; i < 4; ++i) mx = fmaxf(mx, acc[rt][i]);
+            mx = wave_max16(mx);
+            // straight to memory: a 64-byte store per column tile.  The loop's vmcnt
+            // waits still count ring loads correctly: loads complete in issue
+            // order, so while a chunk is pending every later ring load is too,
+            // and an earlier store in flight can only lengthen a wait
+            if (g == 0 && pos < nc) dst[pos] = mx;
           }
-        }
-        const int pos = kChunk * c + c16;
-        if constexpr (ROUGH) {
-          const float sq = row_diff_sq(acc, lane);
-          rough += (pos < nc) ? (double)sq : 0.0;
-        } else {
-          float mx = acc[0][0];
-#pragma unroll
-          for (int rt = 0; rt < 4; ++rt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) mx = fmaxf(mx, acc[rt][i]);
-          mx = wave_max16(mx);
-          // straight to memory: a 64-byte store per chunk.  The loop's vmcnt
-          // waits still count ring loads correctly: loads complete in issue
-          // order, so while a chunk is pending every later ring load is too,
-          // and an earlier store in flight can only lengthen a wait
-          if (g == 0 && pos < nc) dst[pos] = mx;
         }
       }
     }
