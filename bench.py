@@ -34,7 +34,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default=None, choices=["C2", "C3", "C4", "C6"])
+    ap.add_argument("--workload", default=None, choices=["C2", "C3", "C4", "C6", "P7"])
     ap.add_argument("--q", type=float, default=None)
     ap.add_argument("--cpu-units", type=int, default=3072, help="oracle sample size (tile, head units)")
     ap.add_argument("--no-cpu", action="store_true")

@@ -65,7 +65,7 @@ class Workload:
         return dataclasses.replace(self, **kw)
 
 
-# The five single-GPU workloads (attention shapes from Section 4.1; N from
+# The single-GPU workloads (attention shapes from Section 4.1; N from
 # Table 3; selector budgets and q as stated with each).
 WORKLOADS = {
     # tiny: 4 q / 1 kv head, d 64, N 1024, k 4, q 0.25, K-mean, two planted pairs
@@ -81,6 +81,10 @@ WORKLOADS = {
     # Qwen3.6-35B-A3B full-attention layer: 16 q / 2 kv heads, d 256, QK-normed
     # rows, 128K, K-mean (the backbone that wins on this model), k 33, q 0.4
     "C6": Workload("C6", 1, 16, 2, 256, 131072, 33, 0.4, KMEAN, "offset", needles=32, qk_norm=True),
+    # the paper's speed operating point on Qwen2.5-7B-1M (Section 4.3: k_budget
+    # 33, q 0.4, rho 2, router on the winning backbone, Quest on this model),
+    # one layer at 128K
+    "P7": Workload("P7", 1, 28, 4, 128, 131072, 33, 0.4, QUEST, "mixture", needles=32),
 }
 
 
