@@ -96,8 +96,9 @@ def measured_traffic(w, q_override):
 def main():
     a = parse()
     if a.gpus != 1:
-        print(f"bench.py runs on exactly one GPU (asked for --gpus {a.gpus}); the method's "
-              "multi-GPU sharding is described in DESIGN.md but not built", file=sys.stderr)
+        print(f"bench.py runs on exactly one GPU (asked for --gpus {a.gpus}); sharding the path "
+              "across GPUs (by kv-head group) is not built: one GPU's share is what is measured",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
