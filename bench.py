@@ -50,9 +50,11 @@ def parse():
                     help="time the Appendix D diagnostics pass instead (default workload C2)")
     ap.add_argument("--samples", type=int, default=256, help="Monte Carlo samples of the diagnostics")
     ap.add_argument("--oracle-layers", default=None,
-                    help="comma-separated layers of the 28-layer stack: run the oracle on each whole "
-                         "layer (every tile and head), time it and compare with the GPU pipeline")
-    ap.add_argument("--oracle-backbone", default="quest", choices=["quest", "kmean"])
+                    help="comma-separated layers (of --workload, default the 28-layer stack): run the "
+                         "oracle on each whole layer (every tile and head), time it and compare with "
+                         "the GPU pipeline")
+    ap.add_argument("--oracle-backbone", default=None, choices=["quest", "kmean"],
+                    help="backbone for --oracle-layers (default: the workload's own)")
     return ap.parse_args()
 
 
@@ -737,21 +739,26 @@ def _near_tie_ok(g_row, o_row, s_row, t, NB, rel=1e-3):
 
 
 def run_oracle_layers(a, torch, dev, ugbs, synth):
-    """The reference oracle on whole layers of the 28-layer stack (every
-    tile and head): its stage times on the host cores, and the GPU
-    pipeline's kv_idx and output compared with it (kv_idx rows equal up to
-    near-ties, trigger flips only within 1e-3 of tau, attention on the rows
-    with equal lists within max-abs 2e-2 / RMS 2e-3)."""
+    """The reference oracle on whole layers (every tile and head) of a
+    workload (default the 28-layer stack): its stage times on the host
+    cores, and the GPU pipeline's kv_idx and output compared with it
+    (kv_idx rows equal up to near-ties, trigger flips only within 1e-3 of
+    tau, attention on the rows with equal lists within max-abs 2e-2 / RMS
+    2e-3)."""
     import oracle
-    bb = synth.QUEST if a.oracle_backbone == "quest" else synth.KMEAN
-    w = synth.WORKLOADS["C5"].replace(backbone=bb)
+    w = synth.WORKLOADS[a.workload or "C5"]
+    if a.q is not None:
+        w = w.replace(q=a.q)
+    if a.oracle_backbone:
+        w = w.replace(backbone=synth.QUEST if a.oracle_backbone == "quest" else synth.KMEAN)
+    bb_name = "quest" if w.backbone == synth.QUEST else "kmean"
     threads = min(os.cpu_count() or 1, 16)
     res = []
     for layer in [int(x) for x in a.oracle_layers.split(",")]:
         inp = synth.generate(w, layer=layer, threads=16)
         cv = lambda x: torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
         Q, K, V = cv(inp.Q), cv(inp.K), cv(inp.V)
-        p = ugbs.Problem.make(w.B, w.H, w.Hkv, w.N, w.d, w.k, w.q, w.backbone)
+        p = ugbs.Problem.make(w.B, w.H, w.Hkv, w.N, w.d, w.k, w.q, w.backbone, rho=w.rho)
         bufs = ugbs.Buffers(p, device=dev)
         O = torch.empty_like(Q)
         ugbs.prefill(p, Q, K, V, O, bufs)
@@ -766,8 +773,8 @@ def run_oracle_layers(a, torch, dev, ugbs, synth):
         S = oracle.tile_scores(w.backbone, inp.Q, meta, w.Hkv, nthreads=threads)
         t2 = time.perf_counter()
         log(f"oracle layer {layer}: metadata {t1 - t0:.1f}s, tile scores {t2 - t1:.1f}s")
-        idx, sig = oracle.select(S, w.k)
-        kv, sb, tau, trig = oracle.route(sig, idx, w.k, w.q)
+        idx, sig = oracle.select(S, w.k, rho=w.rho)
+        kv, sb, tau, trig = oracle.route(sig, idx, w.k, w.q, rho=w.rho)
         t3 = time.perf_counter()
         log(f"oracle layer {layer}: selection + route {t3 - t2:.1f}s")
         units = oracle.all_units(w.B, w.H, w.T)
@@ -784,7 +791,7 @@ def run_oracle_layers(a, torch, dev, ugbs, synth):
         rows_eq = (g_kv == kv).all(axis=-1)
         bad = 0
         for b, h, t in zip(*np.nonzero(~rows_eq)):
-            width = 2 * w.k if g_trig[b, t] else w.k
+            width = w.rho * w.k if g_trig[b, t] else w.k
             orow = idx[b, h, t].copy()
             orow[width:] = w.NB
             bad += not _near_tie_ok(g_kv[b, h, t], orow, S[b, h, t], int(t), w.NB)
@@ -796,7 +803,7 @@ def run_oracle_layers(a, torch, dev, ugbs, synth):
         f_sc = float(sum(2 * KD * 64 * max(t - 1, 0) for t in range(w.T)) * w.B * w.H)
         f_at = float(sum(4 * w.d * (64 * 64 * (int((r != w.NB).sum()) - 1) + 64 * 65 // 2)
                          for r in kv.reshape(-1, kv.shape[-1])))
-        r = {"layer": layer, "backbone": a.oracle_backbone,
+        r = {"layer": layer, "backbone": bb_name,
              "oracle_seconds": {"meta": round(t1 - t0, 2), "scores": round(t2 - t1, 2),
                                 "select_route": round(t3 - t2, 2), "attend": round(t4 - t3, 2),
                                 "total": round(t4 - t0, 2)},
@@ -809,8 +816,11 @@ def run_oracle_layers(a, torch, dev, ugbs, synth):
         log(f"oracle layer {layer}: {r}")
         res.append(r)
         del S, ref, gO, inp
-    print(json.dumps({"mode": "oracle_full_layers", "workload": "C5: 28-layer stack, 28 q / 4 kv heads, "
-                      "d 128, N 131072, k 64, q 0.1", "host_cpu": _cpu_name(), "layers": res}), flush=True)
+    print(json.dumps({"mode": "oracle_full_layers",
+                      "workload": {"name": w.name, "batch": w.B, "q_heads": w.H, "kv_heads": w.Hkv,
+                                   "head_dim": w.d, "seq_len": w.N, "k_budget": w.k, "q": w.q,
+                                   "rho": w.rho, "backbone": bb_name},
+                      "host_cpu": _cpu_name(), "layers": res}), flush=True)
 
 
 def _cpu_name():
