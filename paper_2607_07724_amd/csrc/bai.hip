@@ -75,7 +75,7 @@ __global__ void __launch_bounds__(64 * kBaiUnits) bai_tile_kernel(TileParams P) 
   const Shape& s = P.s;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int id = xcd_remap(blockIdx.x, P.n_wg);
+  const int id = blockIdx.x;
   if (id >= P.n_wg) return;
   const int hg = id % P.n_hg;
   const int rest = id / P.n_hg;

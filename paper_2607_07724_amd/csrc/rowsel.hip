@@ -122,7 +122,7 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 4, c16 = lane & 15;
   const int n_units = s.B * s.H * s.T;
-  const int uid = xcd_remap(blockIdx.x, n_units);
+  const int uid = blockIdx.x;
   if (uid >= n_units) return;
   const Unit u = unit_of(uid, s);
   const int t = u.t;

@@ -133,8 +133,8 @@ struct MetaChunk {
   __device__ static __forceinline__ int off(int r, int c) { return (r * CPR + (c ^ (r & SWZ))) * 16; }
 };
 
-// Workgroup ordering: the id is XCD-remapped, then (b, kv head) outermost,
-// heaviest tile first, head groups innermost.
+// Workgroup ordering (ids dealt round-robin to the XCDs, see Unit): (b, kv
+// head) outermost, heaviest tile first, head groups innermost.
 struct Group {
   int b, kvh, t, hg;
 };
@@ -195,7 +195,7 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 4, c16 = lane & 15;
 
-  const int id = xcd_remap(blockIdx.x, P.n_wg);
+  const int id = blockIdx.x;
   if (id >= P.n_wg) return;
   const Group gr = group_of(id, P);
   const int hl = gr.hg * P.GW + w;                    // head within the kv head's group
@@ -352,7 +352,7 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int n_units = s.B * s.H * s.T;
   const int n_wg = (n_units + kSelWaves - 1) / kSelWaves;
-  const int wg = xcd_remap(blockIdx.x, n_wg);
+  const int wg = blockIdx.x;
   if (wg >= n_wg) return;
   const int u = wg * kSelWaves + w;
   if (u >= n_units) return;
