@@ -218,8 +218,8 @@ attend_kernel(AttnParams P) {
     const int hpp = (nbh % 2 == 0 && s.T % 4 == 0) ? 2 : 1;   // kv heads in flight
     const int stride = 8 / hpp;                                // XCDs per kv head
     const int n_x = blockIdx.x >> 3, x = blockIdx.x & 7;
-    if (s.T % stride != 0) {                                   // fall back: contiguous ranges per XCD
-      const int uid = xcd_remap(blockIdx.x, P.n_units);
+    if (s.T % stride != 0) {                                   // fall back: units dealt round-robin to the XCDs
+      const int uid = blockIdx.x;
       if (uid >= P.n_units) return;
       u = unit_of(uid, s);
     } else {
