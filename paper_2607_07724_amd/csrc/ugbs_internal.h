@@ -88,18 +88,14 @@ __host__ __device__ inline size_t packed_row(int bh, int t, int T) {
 // adjacent.  The hardware deals consecutive workgroup ids round-robin to the
 // 8 XCDs, so taking the id as the unit index gives every XCD the same mix of
 // heavy and light tiles, with all XCDs on the same kv head (its metadata is
-// read by each XCD's L2).  Contiguous per-XCD ranges (xcd_remap) keep a kv
-// head on one XCD, but are balanced only when a range holds whole kv heads:
-// with 7 or 8 query heads per kv head, or 2 kv heads, they left one XCD the
-// heaviest tiles (scoring 1.4x, per-row selection 1.3-1.5x slower measured).
+// read by each XCD's L2).  Remapping ids to contiguous per-XCD ranges keeps
+// a kv head on one XCD, but is balanced only when a range holds whole kv
+// heads: with 7 or 8 query heads per kv head, or 2 kv heads, it left one XCD
+// the heaviest tiles (scoring 1.4x, per-row selection 1.3-1.5x slower
+// measured).
 struct Unit {
   int b, h, t;
 };
-
-__device__ __forceinline__ int xcd_remap(int id, int n_total) {
-  const int per = (n_total + 7) / 8;
-  return (id % 8) * per + id / 8;
-}
 
 __device__ __forceinline__ Unit unit_of(int u, const Shape& s) {
   Unit r;
