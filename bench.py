@@ -50,9 +50,9 @@ def parse():
                     help="time the Appendix D diagnostics pass instead (default workload C2)")
     ap.add_argument("--samples", type=int, default=256, help="Monte Carlo samples of the diagnostics")
     ap.add_argument("--oracle-layers", default=None,
-                    help="comma-separated layers (of --workload, default the 28-layer stack): run the "
-                         "oracle on each whole layer (every tile and head), time it and compare with "
-                         "the GPU pipeline")
+                    help="CPU-baseline leg over whole layers: comma-separated layers (of --workload, "
+                         "default the 28-layer stack); the oracle runs on each whole layer (every tile "
+                         "and head) on the host cores, is timed, and the GPU pipeline is compared with it")
     ap.add_argument("--oracle-backbone", default=None, choices=["quest", "kmean"],
                     help="backbone for --oracle-layers (default: the workload's own)")
     return ap.parse_args()
@@ -739,9 +739,10 @@ def _near_tie_ok(g_row, o_row, s_row, t, NB, rel=1e-3):
 
 
 def run_oracle_layers(a, torch, dev, ugbs, synth):
-    """The reference oracle on whole layers (every tile and head) of a
-    workload (default the 28-layer stack): its stage times on the host
-    cores, and the GPU pipeline's kv_idx and output compared with it
+    """CPU-baseline leg over whole layers: the reference oracle on every
+    tile and head of a workload's layers (default the 28-layer stack), its
+    stage times on the host cores, and the GPU pipeline's kv_idx and output
+    compared with it
     (kv_idx rows equal up to near-ties, trigger flips only within 1e-3 of
     tau, attention on the rows with equal lists within max-abs 2e-2 / RMS
     2e-3)."""
