@@ -19,7 +19,8 @@
 //
 // Compute, per block and wave (v_mfma_f32_16x16x32_bf16):
 //   S^T = K Q^T   K rows from LDS (ds_read_b128) are the A operand; the
-//                 wave's 32 query rows stay in registers as the B operand;
+//                 wave's query rows (32, or 16 at d = 256) stay in
+//                 registers as the B operand;
 //                 each lane ends up holding 16 keys of one query row.  S of
 //                 the next block is issued together with the softmax of the
 //                 current one, so the matrix cores and the VALU overlap.
