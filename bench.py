@@ -34,7 +34,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default=None, choices=["C2", "C3", "C4", "C6", "P7"])
+    ap.add_argument("--workload", default=None, choices=["C1", "C2", "C3", "C4", "C6", "P7"])
     ap.add_argument("--q", type=float, default=None)
     ap.add_argument("--cpu-units", type=int, default=3072, help="oracle sample size (tile, head units)")
     ap.add_argument("--no-cpu", action="store_true")
@@ -55,6 +55,8 @@ def parse():
                          "and head) on the host cores, is timed, and the GPU pipeline is compared with it")
     ap.add_argument("--oracle-backbone", default=None, choices=["quest", "kmean"],
                     help="backbone for --oracle-layers (default: the workload's own)")
+    ap.add_argument("--oracle-threads", type=int, default=16,
+                    help="host threads for --oracle-layers (1 = the oracle single-threaded)")
     return ap.parse_args()
 
 
@@ -753,7 +755,7 @@ def run_oracle_layers(a, torch, dev, ugbs, synth):
     if a.oracle_backbone:
         w = w.replace(backbone=synth.QUEST if a.oracle_backbone == "quest" else synth.KMEAN)
     bb_name = "quest" if w.backbone == synth.QUEST else "kmean"
-    threads = min(os.cpu_count() or 1, 16)
+    threads = max(1, min(os.cpu_count() or 1, a.oracle_threads))
     res = []
     for layer in [int(x) for x in a.oracle_layers.split(",")]:
         inp = synth.generate(w, layer=layer, threads=16)
