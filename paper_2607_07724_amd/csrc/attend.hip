@@ -459,6 +459,9 @@ attend_kernel(AttnParams P) {
   //   S(i+1) on the matrix cores overlaps the softmax of S(i) on the VALU,
   //   then O += P(i) V(i).  K(i+2) is fetched once S(i+1) is done, V(i+1)
   //   once PV(i) is done.  Fetch order per wave: K0 V0 K1 | K2 V1 | K3 V2 ...
+  //   Two barriers per block: each one both frees a buffer (all waves done
+  //   reading it) and publishes the one load then in flight (V(i) before
+  //   PV(i), K(i+2) before the next S), so every wait is for all loads.
   int blk = listed(0);
   kplan.fetch(Kh + (size_t)blk * Tile<D>::kElems, k_lds, w);
   vplan.fetch(Vh + (size_t)blk * Tile<D>::kElems, v_lds, w);
@@ -468,7 +471,11 @@ attend_kernel(AttnParams P) {
   compute_s(sc);
   wait_lgkm0();
   lds_barrier();                         // all waves are done reading s_k
-  if (n > 1) kplan.fetch(Kh + (size_t)listed(1) * Tile<D>::kElems, k_lds, w);
+  if (n > 1) {
+    kplan.fetch(Kh + (size_t)listed(1) * Tile<D>::kElems, k_lds, w);
+    wait_vmcnt<0>();                     // K1 (and V0) landed
+    lds_barrier();
+  }
 
   // One pipeline step for listed block `it`; MASK: it is the diagonal block
   // (always the last one), whose keys after the query row are masked.
@@ -478,10 +485,6 @@ attend_kernel(AttnParams P) {
     const bool has_next2 = it + 2 < n;
     const int nblk = has_next ? listed(it + 1) : 0;
 
-    if (has_next) {                      // K(it+1) landed (V(it) may be in flight)
-      if (it == 0) wait_vmcnt<0>(); else wait_vmcnt<NW>();
-      lds_barrier();
-    }
     // S(it+1): on the last block this re-reads s_k (no fetch is pending) and is discarded
     f32x4 sn[4][RT];
     __builtin_amdgcn_s_setprio(1);       // matrix-core phases issue ahead of other waves' fetch phases
@@ -549,16 +552,12 @@ attend_kernel(AttnParams P) {
     }
 
     __builtin_amdgcn_s_setprio(0);
-    if (has_next) {
-      wait_lgkm0();
-      lds_barrier();                     // all waves are done reading s_k
-      if (has_next2)
-        kplan.fetch(Kh + (size_t)listed(it + 2) * Tile<D>::kElems, k_lds, w);
-    }
-
-    // V(it) landed (K(it+2) may still be in flight)
-    if (has_next2) wait_vmcnt<NW>(); else wait_vmcnt<0>();
+    // one barrier: every wave is done reading s_k, and V(it), the only load
+    // in flight, has landed
+    wait_lgkm0();
+    wait_vmcnt<0>();
     lds_barrier();
+    if (has_next2) kplan.fetch(Kh + (size_t)listed(it + 2) * Tile<D>::kElems, k_lds, w);
 
     __builtin_amdgcn_s_setprio(1);
     if (__ballot(moved)) {
@@ -594,9 +593,14 @@ attend_kernel(AttnParams P) {
       }
     }
     __builtin_amdgcn_s_setprio(0);
-    wait_lgkm0();
-    lds_barrier();                       // all waves are done reading s_v
-    if (has_next) vplan.fetch(Vh + (size_t)nblk * Tile<D>::kElems, v_lds, w);
+    if (has_next) {
+      // one barrier: every wave is done reading s_v, and K(it+2), the only
+      // load in flight (if any), has landed for the next step's S
+      wait_lgkm0();
+      wait_vmcnt<0>();
+      lds_barrier();
+      vplan.fetch(Vh + (size_t)nblk * Tile<D>::kElems, v_lds, w);
+    }
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
