@@ -54,7 +54,7 @@ struct SelParams {
   float* scratch; // packed candidate scores (workspace), when neither scores_in nor scores_out
   double* rough;  // per-unit row roughness (diagnostics mode of the score kernel)
   int GW;         // waves (query heads) per workgroup of the score kernel
-  int n_groups;   // head groups per kv head = ceil(G / GW)
+  int n_groups;   // score workgroups per (b, kv head) = ceil(T G / GW)
   int n_wg;       // score-kernel workgroups
   int wave_lds;   // bytes of per-wave LDS of the selection kernel (survivors)
   int ring_lds;   // bytes of the metadata ring
@@ -134,17 +134,20 @@ struct MetaChunk {
 };
 
 // Workgroup ordering (ids dealt round-robin to the XCDs, see Unit): (b, kv
-// head) outermost, heaviest tile first, head groups innermost.
+// head) outermost; within it the units (tile, query head) in the order
+// heaviest tile first, sibling heads adjacent, taken GW at a time.  With G
+// a multiple of GW a workgroup holds sibling heads of one tile; otherwise
+// (G = 7: 4 + 3) a workgroup may hold the last heads of tile t and the
+// first of tile t - 1, whose candidate ranges differ by one block, so the
+// metadata chunks are still shared and no wave idles.
 struct Group {
-  int b, kvh, t, hg;
+  int b, kvh, u0;   // u0: the first unit (tile rank * G + head) of the workgroup
 };
 
 __device__ __forceinline__ Group group_of(int id, const SelParams& P) {
   Group r;
-  r.hg = id % P.n_groups;
-  int rest = id / P.n_groups;
-  r.t = P.s.T - 1 - rest % P.s.T;
-  rest /= P.s.T;
+  r.u0 = (id % P.n_groups) * P.GW;
+  const int rest = id / P.n_groups;
   r.kvh = rest % P.s.Hkv;
   r.b = rest / P.s.Hkv;
   return r;
@@ -198,13 +201,17 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
   const int id = blockIdx.x;
   if (id >= P.n_wg) return;
   const Group gr = group_of(id, P);
-  const int hl = gr.hg * P.GW + w;                    // head within the kv head's group
-  const bool active = hl < s.G;
-  const int h = gr.kvh * s.G + (active ? hl : 0);
-  const int t = gr.t;
+  const int x = gr.u0 + w;                            // this wave's unit within the (b, kv head)
+  const bool active = x < s.T * s.G;                  // the last workgroup may be partial
+  const int xs = active ? x : gr.u0;
+  const int h = gr.kvh * s.G + xs % s.G;
+  const int t = s.T - 1 - xs / s.G;
   const size_t row = ((size_t)gr.b * s.H + h) * s.T + t;
-  const int nf = (t == 0) ? 1 : 2;
   const int nc = (t >= 1) ? t - 1 : 0;
+  // the workgroup's heaviest tile (wave 0's) sets the candidate range the
+  // metadata chunks cover; waves of the next tile use one block less
+  const int t_top = s.T - 1 - gr.u0 / s.G;
+  const int nc_top = (t_top >= 1) ? t_top - 1 : 0;
 
   unsigned char* ring = smem;
 
@@ -212,7 +219,7 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
   float* dst = PACKED ? P.scratch + packed_row(gr.b * s.H + h, t, s.T)
                       : (ROUGH ? nullptr : P.scores_out + row * s.NB + 1);
   double rough = 0.0;
-  if (nc > 0) {
+  if (nc_top > 0) {
     // ---- A operand: this wave's 64 query rows (Quest: [q- | q+]) ----------
     // d = 256 Quest: the split pair would take 256 registers per lane, so the
     // raw q rows stay in registers and are split per MFMA (two bit masks)
@@ -241,7 +248,7 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
     // ---- metadata ring: chunk c holds candidate blocks 1 + 16c .. 16c + 16
     const uint16_t* mhead = P.meta + ((size_t)gr.b * s.Hkv + gr.kvh) * s.NB * KD;
     const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(ring));
-    const int nchunks = (nc + MC::kBlocks - 1) / MC::kBlocks;
+    const int nchunks = (nc_top + MC::kBlocks - 1) / MC::kBlocks;
     // this wave issues the chunk's 1 KiB loads i = w, w + GW, ...
     const int n_mine = (MC::kLoads - w + P.GW - 1) / P.GW;
     // this wave's share of a chunk: loads i = w, w + GW, ...; the lane
@@ -251,7 +258,7 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
     auto issue = [&](int c) {
       const uint32_t slot = ring_lds + (uint32_t)((c % kRing) * MC::kBytes);
       const uint16_t* base = mhead + (size_t)__builtin_amdgcn_readfirstlane(1 + MC::kBlocks * c) * KD;
-      const bool last = MC::kBlocks * (c + 1) >= nc;       // wave-uniform
+      const bool last = MC::kBlocks * (c + 1) >= nc_top;   // workgroup-uniform
 #pragma unroll
       for (int j = 0; j < kMaxMine; ++j) {
         const int i = w + j * P.GW;
@@ -260,8 +267,8 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
           const int r = p / MC::CPR;                    // block row within the chunk
           const int col = (p % MC::CPR) ^ (r & MC::SWZ);
           // rows past the last candidate re-read the chunk's first row, which
-          // is a candidate (1 + kBlocks c <= nc for every issued chunk)
-          const int rr = (last && 1 + MC::kBlocks * c + r > nc) ? 0 : r;
+          // is a candidate (1 + kBlocks c <= nc_top for every issued chunk)
+          const int rr = (last && 1 + MC::kBlocks * c + r > nc_top) ? 0 : r;
           const uint32_t off = (uint32_t)((rr * KD + col * 8) * 2);
           dma16(base, off, __builtin_amdgcn_readfirstlane(slot + i * 1024));
         }
@@ -578,8 +585,8 @@ SelParams score_params(const Shape& s, const uint16_t* Q, const uint16_t* meta) 
   P.Q = Q;
   P.meta = meta;
   P.GW = s.G < kMaxGroup ? s.G : kMaxGroup;
-  P.n_groups = (s.G + P.GW - 1) / P.GW;
-  P.n_wg = s.B * s.Hkv * s.T * P.n_groups;
+  P.n_groups = (s.T * s.G + P.GW - 1) / P.GW;   // workgroups per (b, kv head)
+  P.n_wg = s.B * s.Hkv * P.n_groups;
   return P;
 }
 
