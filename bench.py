@@ -180,6 +180,36 @@ def main():
     step_ms = np.array([evs[i][0].elapsed_time(evs[i][4]) for i in range(a.steps)])
     log(f"timed {a.steps} steps: {ms_per_step:.3f} ms/step; stages {np.round(stage_avg, 4).tolist()}")
 
+    # the same layer captured once in a HIP graph and replayed (no host launch
+    # gaps between the kernels); its output must equal the eager layer's
+    graph = None
+    try:
+        O_eager = O.clone()
+        side = torch.cuda.Stream(dev)
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            step()
+        stream.wait_stream(side)
+        torch.cuda.synchronize(dev)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        for _ in range(a.warmup):
+            g.replay()
+        torch.cuda.synchronize(dev)
+        t0 = time.perf_counter()
+        for _ in range(a.steps):
+            g.replay()
+        torch.cuda.synchronize(dev)
+        graph_ms = 1e3 * (time.perf_counter() - t0) / a.steps
+        graph = {"ms_per_step": round(graph_ms, 4),
+                 "output_identical": bool(torch.equal(O.view(torch.int16), O_eager.view(torch.int16)))}
+        del g, O_eager
+        log(f"graph replay: {graph_ms:.3f} ms/step; output identical: {graph['output_identical']}")
+    except Exception as ex:  # reported, never fatal: the eager layer is the measured one
+        graph = {"error": repr(ex)}
+        log(f"graph capture failed: {ex!r}")
+
     # the same layer with the selection inside the attention kernel (no kv_idx lists)
     fb = ugbs.Buffers(p, device=dev)
     Of = torch.empty_like(Q)
@@ -407,6 +437,7 @@ def main():
                           "mean_kept_blocks": round(float(kept_rows.mean()), 3),
                           "needle_hit_rate": float(np.mean(rows_hits)) if rows_hits else None},
         "ms_per_step_median": round(float(np.median(step_ms)), 4),
+        "graph_replay": graph,
         "cold": cold,
         "measured_peaks": probe,
         "stack": stack,
