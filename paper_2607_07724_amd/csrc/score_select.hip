@@ -1,9 +1,10 @@
 // Stages 2+3: tile scores, forcing, sorted top-2k and the cutoff margin
 // (A.2-A.6; Eqs. (tile-score), (sigma-def)).  Two kernels on one stream.
 //
-// score_kernel: one workgroup per (batch, kv head, Q-tile, group of up to 4
-// sibling query heads); each wave owns one query head's unit (64 rows of
-// tile t).  Scoring is a dense contraction on bf16 MFMA
+// score_kernel: one workgroup per 4 consecutive (Q-tile, query head) units
+// of one (batch, kv head), sibling heads of one tile or of two adjacent
+// tiles (see Group); each wave owns one unit (64 rows of its tile).
+// Scoring is a dense contraction on bf16 MFMA
 // (v_mfma_f32_16x16x32_bf16):
 //   S[64 rows x 16 blocks] = Qx[64 x KD] * Mx[KD x 16 blocks]
 // with, for K-mean, Qx = Q and Mx = kbar (KD = d), and for Quest the exact
@@ -14,7 +15,7 @@
 // The wave's 64-row Qx tile stays in registers as the A operand.  Metadata
 // rows (the B operand) come in chunks of 16 or 32 blocks that the workgroup's
 // waves fetch together with direct-to-LDS loads into a 4-slot ring (three
-// chunks in flight), so each chunk crosses L2 once per sibling group; in LDS
+// chunks in flight), so each chunk crosses L2 once per workgroup; in LDS
 // the 16-byte column c of row r sits at c ^ (r mod 16), which makes the
 // operand reads bank-conflict free.  The max over the tile's rows (A.3) is
 // the max over a lane's 16 accumulators and then across the four 16-lane
