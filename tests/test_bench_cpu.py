@@ -1,0 +1,76 @@
+"""Host logic of bench.py: the work counts behind its TFLOP/s figures, the
+staleness rule of the recorded HBM traffic, and the one-GPU contract."""
+import json
+import os
+import subprocess
+import sys
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+from paper_2607_07724_amd import synth  # noqa: E402
+
+
+def _pairs_brute(kv_idx, T):
+    """Attended (query, key) pairs by enumeration: row i of tile t sees key j
+    of a listed block b <= t when 64 b + j <= 64 t + i."""
+    total = 0
+    B, H = kv_idx.shape[:2]
+    for b in range(B):
+        for h in range(H):
+            for t in range(T):
+                blocks = {int(x) for x in kv_idx[b, h, t] if 0 <= x <= t}
+                for blk in blocks:
+                    for i in range(64):
+                        for j in range(64):
+                            total += (64 * blk + j) <= (64 * t + i)
+    return total
+
+
+def test_attention_flops_count_exact_causal_pairs():
+    rng = np.random.default_rng(5)
+    B, H, T, W, d = 1, 2, 9, 4, 64
+    kv = np.full((B, H, T, W), T, np.int32)          # sentinel = N_B
+    for h in range(H):
+        for t in range(T):
+            n = min(W, t + 1)
+            row = rng.choice(t + 1, size=n, replace=False)
+            kv[0, h, t, :n] = row
+    kv[0, 1, 3, -1] = -1                               # junk entries are not attended
+    got = bench.flops_attention(kv, T, d)
+    assert got == 4.0 * d * _pairs_brute(kv, T)
+
+
+def test_score_flops_count_rows_times_candidates():
+    B, H, T, d = 1, 3, 7, 64
+    for backbone, kd in ((0, d), (1, 2 * d)):
+        brute = sum(2 * kd * 64 * max(t - 1, 0) for _ in range(B * H) for t in range(T))
+        assert bench.flops_scores(B, H, T, d, backbone) == brute
+
+
+def test_traffic_record_is_used_only_for_the_source_it_was_taken_on(tmp_path, monkeypatch):
+    (tmp_path / "profiles").mkdir()
+    src_dir = tmp_path / "paper_2607_07724_amd" / "csrc"
+    src_dir.mkdir(parents=True)
+    (src_dir / "attend.hip").write_bytes(b"kernel source A")
+    import hashlib
+    sha = hashlib.sha256(b"kernel source A").hexdigest()
+    rec = {"attend_kernel<128>": {"source_sha256": sha, "fetch_bytes": 100.4, "write_bytes": 20.2}}
+    (tmp_path / "profiles" / "traffic.json").write_text(json.dumps(rec))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    c4 = synth.WORKLOADS["C4"]
+    assert bench.measured_traffic(c4, None) == 121
+    assert bench.measured_traffic(c4, 0.25) is None               # another workload
+    assert bench.measured_traffic(synth.WORKLOADS["C2"], None) is None
+    (src_dir / "attend.hip").write_bytes(b"kernel source B")      # kernel changed since
+    assert bench.measured_traffic(c4, None) is None
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
