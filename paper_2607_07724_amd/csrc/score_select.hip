@@ -414,7 +414,7 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
     }
   }
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  bool filtered = false;
+  bool filtered = false, sort_all = false;
   if (R <= 192 && nc > R) {
     uint32_t top3[3] = {0u, 0u, 0u};
 #pragma unroll
@@ -441,7 +441,22 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
           ns += __popcll(mk);
         }
       }
-      if (ns <= kSurvivors) {
+      if (ns <= 128 && R <= 128) {
+        // few survivors: the register sort below orders all of them, and
+        // the R largest lead (the order (key, ~position) is strict and every
+        // key that can be among the R largest survived), so no exact
+        // threshold search is needed.  Each lane rewrites its own entries
+        // as (key, ~position); unused entries up to 128 become 0.
+        wave_lds_sync();
+#pragma unroll
+        for (int sl = 0; sl < 2; ++sl) {
+          const int i = 64 * sl + lane;
+          const uint64_t v = (i < ns) ? s_sel[i] : 0ull;
+          s_sel[i] = (i < ns) ? ((v & 0xffffffff00000000ull) | (0xffffffffu - (uint32_t)v)) : 0ull;
+        }
+        sort_all = true;
+        filtered = true;
+      } else if (ns <= kSurvivors) {
         wave_lds_sync();
         uint32_t k2[kSurvivors / 64], p2[kSurvivors / 64];
 #pragma unroll
@@ -469,9 +484,10 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
     // partners within a slot are exchanged across lanes, across slots in
     // registers
     wave_lds_sync();
+    const int n_in = sort_all ? 128 : R;   // entries to order (unused ones are 0)
     uint64_t e[2];
-    e[0] = (lane < R) ? s_sel[lane] : 0ull;
-    e[1] = (64 + lane < R) ? s_sel[64 + lane] : 0ull;
+    e[0] = (lane < n_in) ? s_sel[lane] : 0ull;
+    e[1] = (64 + lane < n_in) ? s_sel[64 + lane] : 0ull;
 #pragma unroll
     for (int size = 2; size <= 128; size <<= 1) {
 #pragma unroll
