@@ -9,8 +9,8 @@
 //                 a most-significant-bit-first radix descent (sigma_bar >= 0,
 //                 so its bit pattern is order preserving); trigger[t] is
 //                 (t in P) and sigma_bar[t] <= tau.
-//   route_patch : one thread per kv_idx slot; slots k..2k-1 of tiles that
-//                 do not trigger become the sentinel N_B.
+//   route_patch : one wave per kv_idx row; slots k..W-1 of tiles that do
+//                 not trigger become the sentinel N_B.
 // n_pop and n_trig = ceil(q n_pop) depend only on N, k and q and are
 // computed on the host, so no device-to-host synchronisation is needed.
 #include "ugbs_internal.h"
@@ -53,8 +53,18 @@ __global__ void __launch_bounds__(kStatsThreads) route_stats_kernel(RouteParams 
     uint32_t key = 0xffffffffu;
     if (in_population(t, s.k)) {
 #pragma clang fp contract(off)
+      // fp32 sum in head order; the loads of 8 heads are issued together
+      // before their adds (the order of the adds is unchanged)
+      const float* col = P.sigma + (size_t)b * s.H * s.T + t;
       float acc = 0.0f;
-      for (int h = 0; h < s.H; ++h) acc += P.sigma[((size_t)b * s.H + h) * s.T + t];
+      for (int h0 = 0; h0 < s.H; h0 += 8) {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = (h0 + j < s.H) ? col[(size_t)(h0 + j) * s.T] : 0.0f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (h0 + j < s.H) acc += v[j];
+      }
       sb = __fdiv_rn(acc, (float)s.H);
       if (sb == 0.0f) sb = 0.0f;
       key = __float_as_uint(sb);
@@ -100,20 +110,25 @@ __global__ void __launch_bounds__(kStatsThreads) route_stats_kernel(RouteParams 
   }
 }
 
-__global__ void __launch_bounds__(256) route_patch_kernel(RouteParams P, long n_slots,
+// One wave per kv_idx row (b, h, t), rows grid-strided.  In place only the
+// slots k..W-1 of rows whose tile does not trigger are written.
+__global__ void __launch_bounds__(256) route_patch_kernel(RouteParams P, long n_rows,
                                                           int in_place) {
   const Shape& s = P.s;
-  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n_slots;
-       i += (long)gridDim.x * blockDim.x) {
-    const int slot = (int)(i % s.W);
-    const long row = i / s.W;                 // (b*H + h)*T + t
+  const int lane = threadIdx.x & 63;
+  const long wave0 = (long)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
+  const long n_waves = (long)gridDim.x * (blockDim.x / 64);
+  for (long row = wave0; row < n_rows; row += n_waves) {
     const int t = (int)(row % s.T);
     const int b = (int)(row / ((long)s.T * s.H));
-    const bool keep = slot < s.k || P.ws_trigger[(size_t)b * s.T + t];
+    const bool trig = P.ws_trigger[(size_t)b * s.T + t] != 0;
+    int32_t* dst = P.kv_idx + row * s.W;
     if (in_place) {
-      if (!keep) P.kv_idx[i] = s.NB;
+      if (trig) continue;
+      for (int slot = s.k + lane; slot < s.W; slot += 64) dst[slot] = s.NB;
     } else {
-      P.kv_idx[i] = keep ? P.idx_sorted[i] : s.NB;
+      const int32_t* src = P.idx_sorted + row * s.W;
+      for (int slot = lane; slot < s.W; slot += 64) dst[slot] = (slot < s.k || trig) ? src[slot] : s.NB;
     }
   }
 }
@@ -140,10 +155,10 @@ hipError_t launch_route(const Shape& s, int n_pop, int n_trig, const float* sigm
   route_stats_kernel<<<s.B, kStatsThreads, 0, stream>>>(P);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !kv_idx) return e;  // no lists to patch: flags only
-  const long n_slots = (long)s.B * s.H * s.T * s.W;
-  long blocks = (n_slots + 255) / 256;
+  const long n_rows = (long)s.B * s.H * s.T;
+  long blocks = (n_rows + 3) / 4;
   if (blocks > 65536) blocks = 65536;
-  route_patch_kernel<<<(unsigned)blocks, 256, 0, stream>>>(P, n_slots,
+  route_patch_kernel<<<(unsigned)blocks, 256, 0, stream>>>(P, n_rows,
                                                            idx_sorted == kv_idx ? 1 : 0);
   return hipGetLastError();
 }
