@@ -48,6 +48,10 @@
  *     UGBS_ERR_HIP reports a failed launch (hipGetLastError).
  *   - Inputs must be finite.  Calls on one stream may be issued from any
  *     host thread; the library holds no per-call state.
+ *   - The calls enqueue kernels only (no memset, copy, allocation or
+ *     synchronisation), so a layer can be captured in a HIP graph and
+ *     replayed; make one call of each kind outside the capture first, which
+ *     sets the kernels' LDS limits and caches their occupancy.
  */
 #ifndef UGBS_H
 #define UGBS_H
