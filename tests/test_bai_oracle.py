@@ -280,3 +280,197 @@ def test_mc_mu_rounds_product_and_sum_separately():
     z[0, 2] = zx
     fk, fr = bai.mc_counts(S, 3, np.array([[tau]], f32), z)
     assert fk[0, 0, 6] == 1 and fr[0, 0, 6] == 0
+
+
+# ---------------------------------------------------------------- hand-built pins
+# The tests below feed the aggregate and estimator functions hand-chosen
+# inputs whose outputs follow from the definitions by hand (the expected
+# values are literals, derived in the comments), so that a dropped factor, a
+# quantile taken one position off, or a band taken on sigma instead of g
+# fails.
+
+
+def test_noise_scale_linear_rows_exact():
+    """Recipe step 3 on rows q_r = q_0 + r delta: every adjacent-row
+    difference of the score of block b is delta . m_b, for every tile and
+    every one of the row pairs, so E[(s_{r+1,b} - s_{r,b})^2] is the mean of
+    (delta . m_b)^2 over the (tile, candidate) pairs, and tau^2 is half of
+    it.  The expected value is computed from the dot products alone (no
+    roughness sums, no per-tile pair count)."""
+    d, N, H, Hkv = 64, 64 * 7, 1, 1
+    g = np.random.default_rng(17)
+    q0 = g.integers(1, 9, (H, d)).astype(np.float64)
+    delta = g.integers(-2, 3, (H, d)).astype(np.float64)
+    rows = np.arange(64)[None, :, None]
+    Qf = np.zeros((1, H, N, d))
+    for t in range(N // 64):
+        Qf[0, :, 64 * t:64 * (t + 1)] = q0[:, None, :] + rows * delta[:, None, :]
+    Q = synth.bf16_bits(Qf.astype(np.float32))
+    K = synth.bf16_bits(g.integers(-4, 5, (1, Hkv, N, d)).astype(np.float32))
+    meta = oracle.block_meta(synth.KMEAN, K)
+    sums, terms = oracle.row_roughness(synth.KMEAN, Q, meta, Hkv)
+    kbar = synth.bf16_to_f32(meta).astype(np.float64)[0, 0, :, 0]
+    dots = [float(delta[0] @ kbar[b]) ** 2 for b in range(N // 64)]
+    pairs = [(t, b) for t in range(N // 64) for b in range(1, t)]      # (tile, candidate)
+    want = math.sqrt(sum(dots[b] for _, b in pairs) / len(pairs) / 2.0)
+    assert bai.noise_scale(sums, terms) == pytest.approx(want, rel=1e-15)
+    # a dropped factor 1/2 would give sqrt(2) times this value
+    assert abs(bai.noise_scale(sums, terms) / want - 1.0) < 1e-12
+
+
+def test_noise_scale_recovers_the_noise_model_tau():
+    """Scores s[r, b] = mu_b + tau eps[r, b] with i.i.d. standard normal eps
+    (the noise model of Appendix D with a common mean along the rows):
+    adjacent differences have variance 2 tau^2, so the estimator returns tau
+    up to sampling error (relative standard error 1/sqrt(2 n) for n terms)."""
+    tau = 0.37
+    g = np.random.default_rng(8)
+    n_units, rows, blocks = 40, 64, 30
+    sums, terms = [], []
+    for _ in range(n_units):
+        mu = g.normal(0, 3, blocks)
+        s = mu[None, :] + tau * g.normal(0, 1, (rows, blocks))
+        dif = np.diff(s, axis=0)
+        sums.append(float((dif * dif).sum()))
+        terms.append(dif.size)
+    n = sum(terms)
+    est = bai.noise_scale(np.array(sums), np.array(terms))
+    assert abs(est / tau - 1.0) <= 4.0 / math.sqrt(2.0 * n)
+
+
+def test_tile_gaps_hand_built_tile():
+    """k = 4, rho = 2, tile t = 9: F = [0, 9], m = 2 kept candidates, R' = 6.
+    Candidates (blocks 1..8) sorted: 20, 17, 16.5, 14, 11, 9, 7.5, 6.5, so
+      g = c1 - c2 = 0.5, r = c0 - c2 = 3.5, sigma = 1/7 (fp32 divide),
+      G = c1 - c6 = 17 - 7.5 = 9.5   (rank R' - 1 would give 8, R' + 1 10.5),
+      spacings j = 0..5 without the cut j = 1: 3, 2.5, 3, 2, 1.5 -> delta2 =
+      1.5 (the cut spacing 0.5 and the spacing j = 6 of 1.0 are excluded).
+    Tiles 8 (7 candidates = R' + 1) and 9 are in the mask, tile 7 is not."""
+    k, T = 4, 10
+    s = np.full((1, 1, T, T), -np.inf, np.float32)
+    s[0, 0, 9, 1:9] = [11, 16.5, 6.5, 20, 9, 14, 7.5, 17]
+    s[0, 0, 8, 1:8] = [1, 2, 3, 4, 5, 6, 7]
+    s[0, 0, 7, 1:7] = [1, 2, 3, 4, 5, 6]
+    got = bai.tile_gaps(s, k)
+    assert got["g"][0, 0, 9] == 0.5 and got["r"][0, 0, 9] == 3.5
+    assert got["G"][0, 0, 9] == 9.5
+    assert got["sigma"][0, 0, 9] == np.float32(0.5) / np.float32(3.5)
+    assert got["delta2"][0, 0, 9] == 1.5
+    assert got["valid"][0, 0].tolist() == [False] * 8 + [True, True]
+    # tile 8: sorted 7..1, m = 2: g = 6 - 5, G = 6 - 1 (rank 6), r = 7 - 5
+    assert (got["g"][0, 0, 8], got["G"][0, 0, 8], got["r"][0, 0, 8]) == (1, 5, 2)
+
+
+def _hand_built_heads():
+    """40 valid tiles (tiles 2..41 of T = 42) with
+      r = 1 on the first 20 tiles and 3 on the last 20: mean 2, population
+        standard deviation 1, so r_cv = beta = 0.5 exactly;
+      sigma_i = j_i / 64 with j_i = 11 i mod 40 (a permutation of 0..39);
+      g_i = sigma_i r_i (consistent with sigma = g / r, all exact in fp32);
+      delta2_i = (7 i mod 40 + 1) / 128 (a permutation of 1..40 / 128)."""
+    n, T = 40, 42
+    gaps = {f: np.full((1, 1, T), np.nan, np.float32) for f in ("g", "G", "r", "sigma", "delta2")}
+    gaps["valid"] = np.zeros((1, 1, T), bool)
+    for i in range(n):
+        t = i + 2
+        r = 1.0 if i < 20 else 3.0
+        j = (11 * i) % 40
+        gaps["r"][0, 0, t] = r
+        gaps["sigma"][0, 0, t] = j / 64
+        gaps["g"][0, 0, t] = j / 64 * r
+        gaps["G"][0, 0, t] = j / 64 * r + 1.0
+        gaps["delta2"][0, 0, t] = ((7 * i) % 40 + 1) / 128
+        gaps["valid"][0, 0, t] = True
+    return gaps, n, T
+
+
+def test_head_stats_hand_built_aggregates():
+    """On the hand-built tile set, q = 0.25:
+      n_q = ceil(0.25 * 40) = 10, sigma_(q) = the 10th smallest = 9/64,
+      gamma_q = 9/64 * r_mean = 18/64 = 0.28125;
+      band [gamma (1 - beta), gamma (1 + beta)] = [9/64, 27/64] on g: the
+        r = 1 tiles with j in 9..27 (j = 11, 22, 15, 26, 19, 12, 23, 16, 27,
+        9: ten) and the r = 3 tiles with 3 j in 9..27, i.e. j in 3..9 (j = 6,
+        3, 7: three) -> band mass 13/40 (on sigma it would be 19/40);
+      delta2 quantiles at sorted positions floor(0.05 * 39) = 1 and
+        floor(0.5 * 39) = 19: 2/128 and 20/128; pi_2 = #(delta2 < 2/128)/40
+        = 1/40 (positions 0 or 2 would give 1/128 with pi_2 = 0, or 3/128
+        with pi_2 = 2/40)."""
+    gaps, n, T = _hand_built_heads()
+    fk = np.zeros((1, 1, T), np.int32)
+    fr = np.zeros((1, 1, T), np.int32)
+    st = bai.head_stats(gaps, fk, fr, np.array([[1.0]]), 0.25, 5, 4)
+    assert st["n_tiles"][0, 0] == 40 and st["n_q"][0, 0] == 10
+    assert st["r_mean"][0, 0] == 2.0 and st["r_cv"][0, 0] == 0.5
+    assert st["sigma_q"][0, 0] == 9 / 64 and st["gamma_q"][0, 0] == 0.28125
+    assert st["band_mass"][0, 0] == 13 / 40
+    assert st["delta2_p05"][0, 0] == 2 / 128 and st["delta2_p50"][0, 0] == 20 / 128
+    assert st["pi2"][0, 0] == 1 / 40
+    # Vbar(gamma) = Phi(-gamma / (sqrt2 tau)), against the library CDF
+    nd = statistics.NormalDist()
+    assert st["vbar_gamma"][0, 0] == pytest.approx(nd.cdf(-0.28125 / math.sqrt(2.0)), rel=1e-12)
+
+
+def test_head_stats_bound_branches():
+    """The Proposition's bound min(q, 1 - q) C_q + pi_2 and the band form
+    m_q / 2 C_q + pi_2 in two regimes of the hand-built set:
+      tau = 1 (noise-dominated: Delta_2 = 1/64, chi ~ 1e4, eps_bar > 1):
+        C_q = 1, bound = 0.25 + 1/40 = 0.275, band bound = 13/80 + 1/40;
+      tau = 1e-4 (spacings >> noise: chi = 0, eps_bar = 0, and the band
+        term's density is evaluated 994 standard deviations out): C_q = 0,
+        both bounds = pi_2 = 1/40."""
+    gaps, n, T = _hand_built_heads()
+    z = np.zeros((1, 1, T), np.int32)
+    st = bai.head_stats(gaps, z, z, np.array([[1.0]]), 0.25, 5, 4)
+    assert st["C_q"][0, 0] == 1.0
+    assert st["bound"][0, 0] == pytest.approx(0.275, rel=1e-15)
+    assert st["bound_band"][0, 0] == pytest.approx(13 / 80 + 1 / 40, rel=1e-15)
+    st = bai.head_stats(gaps, z, z, np.array([[1e-4]]), 0.25, 5, 4)
+    assert st["chi"][0, 0] == 0.0 and st["eps_bar"][0, 0] == 0.0 and st["C_q"][0, 0] == 0.0
+    assert st["bound"][0, 0] == 1 / 40 and st["bound_band"][0, 0] == 1 / 40
+    # q = 0.9: min(q, 1 - q) = 0.1, n_q = 36
+    st = bai.head_stats(gaps, z, z, np.array([[1.0]]), 0.9, 5, 4)
+    assert st["n_q"][0, 0] == 36 and st["sigma_q"][0, 0] == 35 / 64
+    assert st["bound"][0, 0] == pytest.approx(0.1 + 1 / 40, rel=1e-14)
+
+
+def test_head_stats_hand_built_monte_carlo():
+    """n_s = 4 samples.  V_t = (fail_k - fail_rk) / n_s.  The router's 10
+    tiles (sigma = 0..9/64) get fail_k = fail_rk = 2 (V = 0); the 10 tiles
+    with sigma = 30..39/64 get fail_k = 4, fail_rk = 0 (V = 1); the rest 0.
+    Regret R_q = (sum of the 10 largest V - sum over the router's tiles) / n
+    = (10 - 0) / 40 = 0.25; mc_err_k = (10 * 2 + 10 * 4) / (40 * 4) = 0.375,
+    mc_err_rk = 20 / 160 = 0.125."""
+    gaps, n, T = _hand_built_heads()
+    fk = np.zeros((1, 1, T), np.int32)
+    fr = np.zeros((1, 1, T), np.int32)
+    for t in range(T):
+        if not gaps["valid"][0, 0, t]:
+            continue
+        j = round(float(gaps["sigma"][0, 0, t]) * 64)
+        if j < 10:
+            fk[0, 0, t] = fr[0, 0, t] = 2
+        elif j >= 30:
+            fk[0, 0, t] = 4
+    st = bai.head_stats(gaps, fk, fr, np.array([[1.0]]), 0.25, 5, 4)
+    assert st["mc_regret"][0, 0] == 0.25
+    assert st["mc_err_k"][0, 0] == 0.375 and st["mc_err_rk"][0, 0] == 0.125
+
+
+@pytest.mark.parametrize("gamma,tau", [(0.3, 1.0), (2.0, 0.7), (0.05, 0.02)])
+def test_C_q_band_term_bounds_the_band_width(gamma, tau):
+    """The band term of C_q bounds the width of the boundary band in Vbar,
+    Vbar(gamma (1 - beta)) - Vbar(gamma (1 + beta)) (proof of the
+    Proposition: the slope phi(x / (sqrt2 tau)) / (sqrt2 tau) integrated
+    over an interval of length 2 beta gamma), and is tight as beta -> 0.
+    With eps_bar = 0 and the other caps inactive, C_q is the band term."""
+    nd = statistics.NormalDist()
+    for beta in (0.5, 0.1, 1e-4):
+        lo = nd.cdf(-gamma * (1 - beta) / (math.sqrt(2.0) * tau))
+        hi = nd.cdf(-gamma * (1 + beta) / (math.sqrt(2.0) * tau))
+        width = lo - hi
+        c = bai.C_q(gamma, beta, tau, 0.0)
+        if c < 0.5:                                  # the band branch is the one taken
+            assert c >= width * (1 - 1e-12)
+            if beta == 1e-4:
+                assert c == pytest.approx(width, rel=1e-3)
