@@ -115,7 +115,15 @@ typedef struct ugbs_problem {
 /* Stage 1 -- block metadata (A.1; Eq. (quest-score) for Quest).
  *   K    : [B, H_kv, N, d] bf16, 16-byte aligned.
  *   meta : UGBS_KMEAN: [B, H_kv, N_B, d] bf16, the mean of the block's 64
- *          keys (exact sum, then rounded to nearest-even bf16).
+ *          keys: the 64 values of a channel are summed in fp64 and the
+ *          mean is rounded once to nearest-even bf16.  The fp64 sum is
+ *          exact (so the result is the correctly rounded exact mean, for
+ *          any order of summation) whenever the nonzero values of the
+ *          channel within the block have binary exponents at most 39
+ *          apart (8 significant bits each, 64 terms: every partial sum then
+ *          fits in 53 bits).  Beyond that range the sum may round in its
+ *          last fp64 bit, which changes the bf16 mean only when it lies
+ *          within that rounding of a bf16 rounding boundary.
  *          UGBS_QUEST: [B, H_kv, N_B, 2, d] bf16, element-wise minimum then
  *          element-wise maximum over the block's 64 keys.
  *          16-byte aligned.  A zero is always written as +0. */

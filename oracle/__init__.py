@@ -24,7 +24,9 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_build.LIB):
+        # rebuilt when missing or older than its source, so a run never loads a stale oracle
+        if (not os.path.exists(_build.LIB)
+                or os.path.getmtime(_build.SRC) > os.path.getmtime(_build.LIB)):
             _build.build()
         L = ctypes.CDLL(_build.LIB)
         P = ctypes.c_void_p

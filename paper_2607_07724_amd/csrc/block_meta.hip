@@ -9,8 +9,9 @@
 // c*d*2 written, c = 1 K-mean, 2 Quest).
 //
 // K-mean: the 64 values of a channel are summed in fp64 (every partial sum
-// is exact for bf16 inputs of ordinary range, so the grouping of the sum
-// does not matter), divided by 64 (exact), and rounded to bf16 once: fp64 -> fp32 with round-to-odd, then fp32 -> bf16 nearest-even,
+// is exact when the nonzero values' binary exponents lie within 39 of each
+// other: 8 significant bits each plus 6 bits of carry fit in 53, so the
+// grouping of the sum does not matter there), divided by 64 (exact), and rounded to bf16 once: fp64 -> fp32 with round-to-odd, then fp32 -> bf16 nearest-even,
 // which equals direct nearest-even rounding because fp32 keeps >= 2 extra
 // bits.  Quest: element-wise fp32 min / max (exact).  Zeros are written +0.
 #include "ugbs_internal.h"

@@ -39,6 +39,18 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, name), name
 
 
+def test_device_code_has_no_packed_fp32():
+    """The gfx950 code of every built object is free of v_pk_add/mul/fma_f32
+    (the build compiles with that target feature off and checks the same;
+    this re-checks the objects the library was linked from)."""
+    from paper_2607_07724_amd import build
+    objs = [os.path.join(build.BUILD, os.path.splitext(s)[0] + ".o") for s in build.SOURCES]
+    if not all(os.path.exists(o) for o in objs):
+        pytest.skip("objects not built here (run __graft_entry__.build())")
+    scanned = sum(build.check_no_packed_fp32(o) for o in objs)
+    assert scanned > 10000
+
+
 def test_abi_version_and_status_strings():
     assert ugbs.ugbs_abi_version() == _enum("UGBS_ABI_VERSION")
     for st in range(10):

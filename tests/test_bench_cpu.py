@@ -74,3 +74,55 @@ def test_more_than_one_gpu_is_refused_with_a_message():
     assert r.returncode == 2
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+def test_selection_stats_by_hand():
+    """Two kv heads x two sibling query heads, three population tiles
+    (k = 1 so every tile t >= 1 is in it); lists chosen so every overlap is
+    known: head 0 keeps {0,1} at every tile, head 1 {0,2} at tiles 1-2 and
+    {0,1} at tile 3, heads 2/3 (the second kv head) identical lists {1, 2}."""
+    w = synth.Workload("t", 1, 4, 2, 64, 64 * 4, 1, 0.5, 0, "offset")
+    NB = w.NB
+    kv = np.full((1, 4, 4, 2), NB, np.int32)
+    kv[0, 0, :] = [0, 1]
+    kv[0, 1, :] = [0, 2]
+    kv[0, 1, 3] = [0, 1]
+    kv[0, 2:, :] = [1, 2]
+    trig = np.zeros((1, 4), np.uint8)
+    st = bench.selection_stats(kv, trig, w)
+    assert st["mean_kept_blocks"] == 2.0
+    # adjacent tiles (1,2), (2,3) of every head: 1, 1/3 for head 1, 1 otherwise
+    assert st["jaccard_adjacent_tiles"] == round((6 * 1 + 1 + 1 / 3) / 8, 4)
+    # sibling pairs at tiles 1..3: kv head 0: 1/3, 1/3, 1; kv head 1: 1, 1, 1
+    assert st["jaccard_sibling_heads"] == round((1 / 3 + 1 / 3 + 1 + 3) / 6, 4)
+    # unions: kv head 0 {0,1,2},{0,1,2},{0,1}; kv head 1 {1,2} x3; lists sum 4 each
+    assert st["sibling_union_blocks"] == round((3 + 3 + 2 + 2 + 2 + 2) / 6, 2)
+    assert st["sibling_union_over_sum"] == round(14 / 24, 4)
+
+
+def test_cpu_leg_parity_on_oracle_outputs():
+    """The CPU leg's parity check, fed the oracle's own routed lists and its
+    attention rounded to bf16 as the 'GPU' result, reports every sampled row
+    equal and the output within tolerance; a planted wrong block fails it."""
+    import oracle
+    w = synth.WORKLOADS["C1"]
+    inp = synth.generate(w, threads=4)
+    meta = oracle.block_meta(w.backbone, inp.K)
+    S = oracle.tile_scores(w.backbone, inp.Q, meta, w.Hkv)
+    idx, sig = oracle.select(S, w.k)
+    kv, sb, tau, trig = oracle.route(sig, idx, w.k, w.q)
+    units = bench.cpu_sample_units(w, 24)
+    ref = oracle.attend(inp.Q, inp.K, inp.V, kv_idx=kv)
+    O_units = np.stack([synth.bf16_bits(ref[b, h, 64 * t:64 * t + 64].astype(np.float32))
+                        for b, h, t in units])
+    r = bench.cpu_baseline(w, inp, units, kv, trig.astype(np.uint8), O_units, threads=2)
+    assert r["parity"]["ok"] and r["parity"]["kv_rows_equal"] == len(units)
+    assert r["cores"] == 2 and r["host_logical_cpus"] >= 1
+    b, h, t = units[0]
+    bad = kv.copy()
+    row = [x for x in bad[b, h, t] if x != w.NB]
+    spare = [x for x in range(1, t) if x not in row]
+    if spare:
+        bad[b, h, t, len(row) - 1] = spare[-1]
+        r2 = bench.cpu_baseline(w, inp, units, bad, trig.astype(np.uint8), O_units, threads=2)
+        assert r2["parity"]["kv_rows_beyond_near_ties"] >= 1 and not r2["parity"]["ok"]

@@ -329,21 +329,21 @@ def test_end_to_end_against_oracle(name):
                 width = w.rho * k if g["trig"][b, t] else k
                 orc_row = c["idx"][b, h, t].copy()
                 orc_row[width:] = NB
-                ok, nd = near_tie_ok(g["kv"][b, h, t], orc_row, c["S"][b, h, t], t, NB)
+                ok, nd = near_tie_ok(g["kv"][b, h, t], orc_row, c["S"][b, h, t], t, NB, k)
                 assert ok, (b, h, t, g["kv"][b, h, t], orc_row)
                 if nd:
                     exempt += 1
                 rows_equal[b, h, t] = np.array_equal(g["kv"][b, h, t], c["kv"][b, h, t])
     print(f"{name}: near-tie exemptions {exempt}, rows equal {rows_equal.mean():.4f}")
-    # attention where the kept lists agree with the oracle's
-    O = bf16_to_f64(g["O"])
-    ref = oracle.attend(inp.Q, inp.K, inp.V, kv_idx=c["kv"])
-    for b in range(w.B):
-        for h in range(w.H):
-            for t in range(w.T):
-                if rows_equal[b, h, t]:
-                    d = O[b, h, 64 * t:64 * t + 64] - ref[b, h, 64 * t:64 * t + 64]
-                    assert np.abs(d).max() <= ATOL_MAX
+    # attention: against the oracle's exact attention over the GPU's own kept
+    # lists on every row, and over the oracle's lists where the two agree
+    ref = oracle.attend(inp.Q, inp.K, inp.V, kv_idx=g["kv"])
+    mx, rms = attention_error(g["O"], ref)
+    assert mx <= ATOL_MAX and rms <= ATOL_RMS, (mx, rms)
+    ref_o = oracle.attend(inp.Q, inp.K, inp.V, kv_idx=c["kv"])
+    rows = np.repeat(rows_equal, 64, axis=-1)
+    d = bf16_to_f64(g["O"])[rows] - ref_o[rows]
+    assert np.abs(d).max() <= ATOL_MAX and np.sqrt(np.mean(d * d)) <= ATOL_RMS
     assert rows_equal.mean() > 0.9
 
 

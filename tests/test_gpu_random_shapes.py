@@ -124,7 +124,7 @@ def test_random_shape_against_oracle(seed):
                 width = w.rho * w.k if etrig[b, t] else w.k
                 orow = idx[b, h, t].copy()
                 orow[width:] = w.NB
-                ok, _ = near_tie_ok(ekv[b, h, t], orow, S[b, h, t], t, w.NB)
+                ok, _ = near_tie_ok(ekv[b, h, t], orow, S[b, h, t], t, w.NB, w.k)
                 assert ok, (b, h, t, ekv[b, h, t], orow)
 
     # the selection inside the attention kernel: same output as the lists path

@@ -88,6 +88,27 @@ def test_kmean_is_exact_mean_rounded_to_nearest_even():
         assert meta[b, kvh, blk, 0, e] == _nearest_bf16_exact(exact)
 
 
+def test_kmean_exact_at_the_widest_exact_exponent_range():
+    """The fp64 sum of a channel's 64 bf16 values is exact when their binary
+    exponents lie within 39 of each other (8 significant bits plus 6 bits of
+    carry in 53): channels mixing magnitudes 2^20 and 2^-19 of both signs,
+    whose exact mean needs every low bit, still round to the nearest-even
+    bf16 of the exact rational mean."""
+    g = np.random.default_rng(12)
+    N, d = 2 * BLK, 16
+    mant = 1.0 + g.integers(0, 128, (1, 1, N, d)) / 128.0
+    expo = np.where(g.random((1, 1, N, d)) < 0.5, 20, -19)
+    sign = np.where(g.random((1, 1, N, d)) < 0.5, -1.0, 1.0)
+    K = synth.bf16_bits((sign * mant * np.exp2(expo)).astype(np.float32))
+    meta = oracle.block_meta(oracle.KMEAN, K)
+    Kf = f32(K)
+    for blk in range(N // BLK):
+        for e in range(d):
+            col = Kf[0, 0, blk * BLK:(blk + 1) * BLK, e]
+            exact = sum(Fraction(float(v)) for v in col) / BLK
+            assert meta[0, 0, blk, 0, e] == _nearest_bf16_exact(exact)
+
+
 def test_quest_min_max_bound_every_key_and_are_attained():
     inp = small_inputs(keys="mixture")
     meta = oracle.block_meta(oracle.QUEST, inp.K)
