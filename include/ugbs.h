@@ -69,11 +69,12 @@ extern "C" {
 #define UGBS_API
 #endif
 
-#define UGBS_ABI_VERSION 6
+#define UGBS_ABI_VERSION 7
 #define UGBS_BLOCK 64          /* BLOCK_M = BLOCK_N = 64 tokens (Section 3.1, 3.2) */
 #define UGBS_MAX_BLOCKS 2048   /* N_B <= 2048, i.e. N <= 131072 */
 #define UGBS_MAX_KV_WIDTH 4096 /* kv_width accepted by ugbs_attend; rho * k_budget <= 4096 */
 #define UGBS_MAX_RHO 8         /* expansion factor rho in 1..8 */
+#define UGBS_ROUTE_SCRATCH_BYTES (1u << 20) /* device scratch of ugbs_route_noalloc, per GPU */
 
 typedef enum {
   UGBS_OK = 0,
@@ -85,7 +86,8 @@ typedef enum {
   UGBS_ERR_ALIGN = 6,     /* a pointer is not aligned as documented */
   UGBS_ERR_WORKSPACE = 7, /* workspace NULL or smaller than ugbs_workspace_bytes */
   UGBS_ERR_HIP = 8,       /* a HIP launch failed */
-  UGBS_ERR_SCALE = 9      /* softmax_scale negative, NaN or infinite */
+  UGBS_ERR_SCALE = 9,     /* softmax_scale negative, NaN or infinite */
+  UGBS_ERR_SCRATCH = 10   /* the problem needs more than the static scratch of ugbs_route_noalloc */
 } ugbs_status;
 
 /* Block-scoring backbone (Section 3.1).
@@ -193,6 +195,33 @@ UGBS_API int ugbs_score_select(const ugbs_problem* p, const void* Q, const void*
 UGBS_API int ugbs_route(const ugbs_problem* p, const float* sigma, const int32_t* idx_sorted,
                int32_t* kv_idx, float* sigma_bar, float* tau, uint8_t* trigger,
                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Stage 4 for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation):
+ * ugbs_route without a workspace argument.  Same arguments and results as
+ * ugbs_route (every output bit-identical); the route's own sections
+ * (sigma_bar | tau | trigger, each 256-byte aligned: 4 B T + 4 B + B T bytes
+ * rounded up) live in a static device array of UGBS_ROUTE_SCRATCH_BYTES
+ * (1 MiB) that the library holds on each GPU it runs on until the process
+ * ends; any batch up to 64 at every supported N fits.  A problem whose
+ * sections exceed it returns UGBS_ERR_SCRATCH before anything is enqueued.
+ * The call allocates nothing (no hipMalloc, no allocating library routine);
+ * on its first call on a device it looks up that device's copy of the array
+ * (the current device, which `stream` must belong to).
+ *   - Every call on a GPU shares that GPU's array, which keeps the last
+ *     call's contents; calls that overlap in time on one GPU (other streams,
+ *     other host threads) race on it and must be ordered by the caller.
+ *   - The array is written in full for the problem's sections before it is
+ *     read, so no clearing is needed between calls.
+ *   - The trigger flags stay in the library's array, not in a caller
+ *     workspace: a following ugbs_attend_select takes them through its
+ *     `trigger` argument (pass this call's `trigger` output).
+ * With ugbs_score_select given scores_out (no workspace needed), a layer
+ * runs without any workspace: block_meta, score_select, route_noalloc,
+ * attend. */
+UGBS_API int ugbs_route_noalloc(const ugbs_problem* p, const float* sigma, const int32_t* idx_sorted,
+                                int32_t* kv_idx, float* sigma_bar, float* tau, uint8_t* trigger,
+                                void* stream);
 
 /* Stage 5 -- block-sparse causal attention over kv_idx (A.10; Eq. (Attn)).
  *   For row i of tile t and query head h, the attended keys are

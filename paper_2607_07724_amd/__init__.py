@@ -22,13 +22,14 @@ __all__ = [
     "ugbs_workspace_bytes", "ugbs_status_string", "ugbs_abi_version",
     "ugbs_attend_select", "prefill_fused", "ugbs_select_rows", "ugbs_attend_bitmap",
     "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads", "BAI_TILE_FIELDS", "BAI_HEAD_FIELDS",
-    "bai_tile_records", "bai_head_records",
+    "bai_tile_records", "bai_head_records", "ugbs_route_noalloc", "ROUTE_SCRATCH_BYTES",
 ]
 
 KMEAN, QUEST = 0, 1
 BLOCK = 64
 MAX_BLOCKS = 2048
 MAX_KV_WIDTH = 4096
+ROUTE_SCRATCH_BYTES = 1 << 20
 _HERE = os.path.dirname(os.path.abspath(__file__))
 
 
@@ -101,6 +102,7 @@ def lib():
         L.ugbs_block_meta.argtypes = [pp, P, P, P]
         L.ugbs_score_select.argtypes = [pp, P, P, P, P, P, P, P, ctypes.c_size_t, P]
         L.ugbs_route.argtypes = [pp, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+        L.ugbs_route_noalloc.argtypes = [pp, P, P, P, P, P, P, P]
         L.ugbs_attend.argtypes = [pp, P, P, P, P, ctypes.c_int32, P, P]
         L.ugbs_workspace_bytes.argtypes = [pp]
         L.ugbs_workspace_bytes.restype = ctypes.c_size_t
@@ -115,7 +117,7 @@ def lib():
         L.ugbs_bai_heads.argtypes = [pp, P, P, ctypes.c_int32, P, P]
         for f in ("ugbs_block_meta", "ugbs_score_select", "ugbs_route", "ugbs_attend", "ugbs_abi_version",
                   "ugbs_attend_select", "ugbs_select_rows", "ugbs_attend_bitmap",
-                  "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads"):
+                  "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads", "ugbs_route_noalloc"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -225,6 +227,25 @@ def ugbs_route(p: Problem, sigma, idx_sorted, kv_idx, workspace, sigma_bar=None,
     _raise("ugbs_route", lib().ugbs_route(ctypes.byref(p), sg, ix, kv, sb, ta, tr, ws,
                                           workspace.numel() * workspace.element_size(),
                                           _stream(stream)))
+
+
+def ugbs_route_noalloc(p: Problem, sigma, idx_sorted, kv_idx, sigma_bar=None, tau=None, trigger=None,
+                       stream=None):
+    """Stage 4 without a workspace (for callers that cannot allocate): the
+    route's sections live in the library's static per-GPU scratch; outputs
+    equal ugbs_route's."""
+    import torch
+    dev = sigma.device
+    sg = _check("sigma", sigma, (p.batch, p.n_heads, p.T), (torch.float32,))
+    if (idx_sorted is None) != (kv_idx is None):
+        raise ValueError("idx_sorted and kv_idx are given together or not at all")
+    ix = _opt("idx_sorted", idx_sorted, (p.batch, p.n_heads, p.T, p.W), (torch.int32,), dev)
+    kv = _opt("kv_idx", kv_idx, (p.batch, p.n_heads, p.T, p.W), (torch.int32,), dev)
+    sb = _opt("sigma_bar", sigma_bar, (p.batch, p.T), (torch.float32,), dev)
+    ta = _opt("tau", tau, (p.batch,), (torch.float32,), dev)
+    tr = _opt("trigger", trigger, (p.batch, p.T), (torch.uint8,), dev)
+    _raise("ugbs_route_noalloc", lib().ugbs_route_noalloc(ctypes.byref(p), sg, ix, kv, sb, ta, tr,
+                                                          _stream(stream)))
 
 
 def ugbs_attend(p: Problem, Q, K, V, kv_idx, O, stream=None):

@@ -77,6 +77,7 @@ const char* ugbs_status_string(int status) {
     case UGBS_ERR_WORKSPACE: return "workspace missing or too small";
     case UGBS_ERR_HIP: return "HIP launch failed";
     case UGBS_ERR_SCALE: return "softmax_scale negative or not finite";
+    case UGBS_ERR_SCRATCH: return "problem exceeds the static scratch of ugbs_route_noalloc";
     default: return "unknown status";
   }
 }
@@ -131,6 +132,25 @@ int ugbs_route(const ugbs_problem* p, const float* sigma, const int32_t* idx_sor
   const int n_trig = (int)std::ceil(s.q * (double)n_pop);
   return hip_status(ugbs::launch_route(s, n_pop, n_trig, sigma, idx_sorted, kv_idx, sigma_bar,
                                        tau, trigger, workspace,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+int ugbs_route_noalloc(const ugbs_problem* p, const float* sigma, const int32_t* idx_sorted,
+                       int32_t* kv_idx, float* sigma_bar, float* tau, uint8_t* trigger, void* stream) {
+  Shape s;
+  int st = make_shape(p, &s);
+  if (st) return st;
+  if (!sigma || (!idx_sorted != !kv_idx)) return UGBS_ERR_NULL;
+  if (!aligned(sigma, 4) || !aligned(idx_sorted, 4) || !aligned(kv_idx, 4) ||
+      !aligned(sigma_bar, 4) || !aligned(tau, 4))
+    return UGBS_ERR_ALIGN;
+  if (ugbs::ws_route_total(s) > ugbs::kRouteScratchBytes) return UGBS_ERR_SCRATCH;
+  void* scratch_ptr = nullptr;
+  if (ugbs::route_scratch(&scratch_ptr) != hipSuccess) return UGBS_ERR_HIP;
+  const int n_pop = population_size(s);
+  const int n_trig = (int)std::ceil(s.q * (double)n_pop);
+  return hip_status(ugbs::launch_route(s, n_pop, n_trig, sigma, idx_sorted, kv_idx, sigma_bar,
+                                       tau, trigger, scratch_ptr,
                                        static_cast<hipStream_t>(stream)));
 }
 

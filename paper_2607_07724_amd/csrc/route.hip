@@ -13,6 +13,8 @@
 //                 not trigger become the sentinel N_B.
 // n_pop and n_trig = ceil(q n_pop) depend only on N, k and q and are
 // computed on the host, so no device-to-host synchronisation is needed.
+#include <mutex>
+
 #include "ugbs_internal.h"
 
 namespace ugbs {
@@ -133,7 +135,36 @@ __global__ void __launch_bounds__(256) route_patch_kernel(RouteParams P, long n_
   }
 }
 
+// Route sections (sigma_bar | tau | trigger) of ugbs_route_noalloc, in device
+// memory the library owns: one copy of this array per GPU, held until the
+// process ends.  Host code must not pass `scratch` itself to a kernel (on the
+// host it names a stand-in, not a device address); the per-device address
+// comes from hipGetSymbolAddress below.
+static __device__ __align__(256) unsigned char scratch[kRouteScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];   // device address of `scratch`, per device
+
 }  // namespace
+
+// Device address of the current device's `scratch`, looked up once per
+// device with that device current.
+hipError_t route_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_route(const Shape& s, int n_pop, int n_trig, const float* sigma,
                         const int32_t* idx_sorted, int32_t* kv_idx, float* sigma_bar,

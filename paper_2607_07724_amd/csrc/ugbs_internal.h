@@ -35,6 +35,11 @@ size_t score_scratch_bytes(const Shape& s);
 hipError_t launch_route(const Shape& s, int n_pop, int n_trig, const float* sigma,
                         const int32_t* idx_sorted, int32_t* kv_idx, float* sigma_bar,
                         float* tau, uint8_t* trigger, void* workspace, hipStream_t stream);
+// The route without a caller's workspace: its sections live in a static
+// device array of kRouteScratchBytes per GPU (route.hip); route_scratch gives
+// the current device's address of it.
+constexpr size_t kRouteScratchBytes = UGBS_ROUTE_SCRATCH_BYTES;
+hipError_t route_scratch(void** ptr);
 // Per-row selection into tile bitmaps, and attention over bitmaps.
 hipError_t launch_select_rows(const Shape& s, const uint16_t* Q, const uint16_t* meta,
                               const float* row_scores, const uint8_t* trigger, uint32_t* bitmap,

@@ -53,7 +53,7 @@ def test_device_code_has_no_packed_fp32():
 
 def test_abi_version_and_status_strings():
     assert ugbs.ugbs_abi_version() == _enum("UGBS_ABI_VERSION")
-    for st in range(10):
+    for st in range(11):
         s = ugbs.ugbs_status_string(st)
         assert s and s != "unknown status"
     assert ugbs.ugbs_status_string(12345) == "unknown status"
@@ -104,6 +104,7 @@ def test_invalid_problem_rejected_by_every_entry_point(kw, code):
     assert L.ugbs_block_meta(ctypes.byref(p), fake, fake, None) == want
     assert L.ugbs_score_select(ctypes.byref(p), fake, fake, None, None, fake, fake, fake, 1 << 30, None) == want
     assert L.ugbs_route(ctypes.byref(p), fake, fake, fake, None, None, None, fake, 1 << 20, None) == want
+    assert L.ugbs_route_noalloc(ctypes.byref(p), fake, fake, fake, None, None, None, None) == want
     assert L.ugbs_attend(ctypes.byref(p), fake, fake, fake, fake, 8, fake, None) == want
     assert L.ugbs_attend_select(ctypes.byref(p), fake, fake, fake, None, None, fake, 1 << 30, fake, None) == want
     assert L.ugbs_workspace_bytes(ctypes.byref(p)) == 0
@@ -125,6 +126,10 @@ def test_null_problem_and_null_pointers():
     assert L.ugbs_route(ctypes.byref(p), None, fake, fake, None, None, None, fake, 1 << 20, None) == ERR_NULL
     assert L.ugbs_route(ctypes.byref(p), fake, fake, None, None, None, None, fake, 1 << 20, None) == ERR_NULL
     assert L.ugbs_route(ctypes.byref(p), fake, None, fake, None, None, None, fake, 1 << 20, None) == ERR_NULL
+    assert L.ugbs_route_noalloc(ctypes.byref(p), None, fake, fake, None, None, None, None) == ERR_NULL
+    assert L.ugbs_route_noalloc(ctypes.byref(p), fake, fake, None, None, None, None, None) == ERR_NULL
+    assert L.ugbs_route_noalloc(ctypes.byref(p), fake, None, fake, None, None, None, None) == ERR_NULL
+    assert L.ugbs_route_noalloc(None, fake, fake, fake, None, None, None, None) == ERR_NULL
     for i in range(4):
         args = [fake] * 4
         args[i] = None
@@ -316,3 +321,27 @@ def test_row_selection_and_bitmap_attention_checks():
     assert L.ugbs_select_rows(ctypes.byref(bad), fake, fake, None, fake, fake, None) == _enum("UGBS_ERR_BUDGET")
     assert L.ugbs_attend_bitmap(ctypes.byref(good(head_dim=96)), fake, fake, fake, fake, fake,
                                 None) == _enum("UGBS_ERR_SHAPE")
+
+
+def test_route_noalloc_scratch_limit_and_alignment():
+    """The allocation-free route rejects, before touching the device, a
+    problem whose route sections (4 B T + 4 B + B T bytes, each rounded up
+    to 256) exceed its 1 MiB static scratch; batch 64 at N = 131072 fits,
+    batch 128 does not."""
+    L = ugbs.lib()
+    fake = ctypes.c_void_p(0x100000)
+    ERR_SCRATCH, ERR_ALIGN = _enum("UGBS_ERR_SCRATCH"), _enum("UGBS_ERR_ALIGN")
+    assert ugbs.ROUTE_SCRATCH_BYTES == 1 << 20
+
+    def sections(B, T):
+        al = lambda x: (x + 255) // 256 * 256
+        return al(4 * B * T) + al(4 * B) + al(B * T)
+
+    assert sections(64, 2048) <= 1 << 20 < sections(128, 2048)
+    big = ugbs.Problem.make(128, 4, 1, 131072, 64, 4, 0.25, ugbs.KMEAN)
+    assert L.ugbs_route_noalloc(ctypes.byref(big), fake, fake, fake, None, None, None, None) == ERR_SCRATCH
+    assert L.ugbs_route_noalloc(ctypes.byref(big), fake, None, None, None, None, None, None) == ERR_SCRATCH
+    p = good()
+    odd = ctypes.c_void_p(0x100002)
+    assert L.ugbs_route_noalloc(ctypes.byref(p), odd, fake, fake, None, None, None, None) == ERR_ALIGN
+    assert L.ugbs_route_noalloc(ctypes.byref(p), fake, fake, fake, odd, None, None, None) == ERR_ALIGN
