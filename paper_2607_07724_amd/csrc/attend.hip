@@ -225,14 +225,13 @@ attend_kernel(AttnParams P) {
           const uint32_t t0 = kth_largest<3>(top3, 3, R, &exact0);
           constexpr int kSurv = 256;
           uint64_t* s_surv = reinterpret_cast<uint64_t*>(s_k);
-          const uint64_t ltm = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
           int ns = 0;
 #pragma unroll
           for (int sl = 0; sl < kSlots; ++sl) {
             if (sl < nslots) {
               const bool tk = t0 > 0u && keys[sl] >= t0;
               const uint64_t mk = __ballot(tk);
-              const int at = ns + __popcll(mk & ltm);
+              const int at = ns + lanes_below(mk);
               if (tk && at < kSurv) s_surv[at] = ((uint64_t)keys[sl] << 32) | (uint32_t)(64 * sl + lane);
               ns += __popcll(mk);
             }
@@ -264,13 +263,12 @@ attend_kernel(AttnParams P) {
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_wave_barrier();
-    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     int n = 0, below = 0;
     for (int base = 0; base <= u.t; base += 64) {
       const int blk = base + lane;
       const bool on = blk <= u.t && ((s_bits[blk >> 5] >> (blk & 31)) & 1u);
       const uint64_t m = __ballot(on);
-      if (on) s_list[n + __popcll(m & lt)] = blk;
+      if (on) s_list[n + lanes_below(m)] = blk;
       n += __popcll(m);
       below += __popcll(__ballot(on && blk < start_blk));
     }

@@ -327,7 +327,6 @@ __global__ void __launch_bounds__(kHeadThreads) bai_head_kernel(HeadParams P) {
 
   // ---- compact the valid tiles in tile order (wave 0) ---------------------
   if (tid < 64) {
-    const uint64_t lt_mask = (tid == 0) ? 0ull : (~0ull >> (64 - tid));
     int base = 0;
     for (int t0 = 0; t0 < s.T; t0 += 64) {
       const int t = t0 + tid;
@@ -335,7 +334,7 @@ __global__ void __launch_bounds__(kHeadThreads) bai_head_kernel(HeadParams P) {
       const bool v = t < s.T && (x = tl[t], x.valid != 0);
       const uint64_t mk = __ballot(v);
       if (v) {
-        const int i = base + __popcll(mk & lt_mask);
+        const int i = base + lanes_below(mk);
         s_sig[i] = x.sigma;
         s_g[i] = x.g;
         s_r[i] = x.r;

@@ -71,14 +71,13 @@ __device__ __forceinline__ void row_top(const float* row, int nc, int R, int lan
     const uint32_t t0 = kth_largest<3>(top3, 3, R, &exact0);
     constexpr int kSurv = kSurvivors;
     wave_lds_sync();  // the row's keys are in registers: s_surv may reuse its space
-    const uint64_t ltm = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     int ns = 0;
 #pragma unroll
     for (int sl = 0; sl < kRowSlots; ++sl) {
       if (sl < nslots) {
         const bool tk = t0 > 0u && keys[sl] >= t0;
         const uint64_t mk = __ballot(tk);
-        const int at = ns + __popcll(mk & ltm);
+        const int at = ns + lanes_below(mk);
         if (tk && at < kSurv) s_surv[at] = ((uint64_t)keys[sl] << 32) | (uint32_t)(64 * sl + lane);
         ns += __popcll(mk);
       }

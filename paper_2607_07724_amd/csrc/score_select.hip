@@ -25,13 +25,16 @@
 //
 // select_kernel: one wave per unit, heaviest tile first.  Tile scores
 // become order-preserving 32-bit keys (-0 folded into +0).  A per-lane
-// top-2 pre-filter bounds the R-th largest key from below (R = min(2k -
-// |F|, |C|)), the R-th largest key is found among the survivors by a
+// top-3 pre-filter bounds the R-th largest key from below (R = min(max(W -
+// |F|, m + 1), |C|): the listed candidates, and at least the m + 1 that
+// sigma needs), the R-th largest key is found among the survivors by a
 // most-significant-bit-first radix descent that counts with wave ballots,
 // the top R are compacted (equal keys at the threshold by lower block
 // index) and ordered by (key, ~index) with a bitonic sort: in registers
 // across lanes for R <= 128, in LDS above.  sigma uses IEEE fp32 subtract and
-// divide.  Splitting the stages keeps each kernel at its own occupancy (the
+// divide.  The kernel is bound by instruction issue, not by its reads: on
+// the 128K layer about 1600 VALU instructions per unit keep the VALU active
+// for ~87% of the SIMD cycles.  Splitting the stages keeps each kernel at its own occupancy (the
 // scoring kernel is bound by registers, the selection kernel by latency).
 #include "select_common.h"
 
@@ -413,18 +416,17 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
       keys[sl] = (sl < nslots && p < nc) ? order_key(raw[sl]) : 0u;  // valid keys are >= 0x007fffff
     }
   }
-  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   bool filtered = false, sort_all = false;
   if (R <= 192 && nc > R) {
+    // (slots past the row hold key 0, the smallest: no guard needed here or
+    // in the compaction below, where only keys >= t0 > 0 are taken)
     uint32_t top3[3] = {0u, 0u, 0u};
 #pragma unroll
     for (int sl = 0; sl < kMaxSlots; ++sl) {
-      if (sl < nslots) {
-        const uint32_t x = keys[sl];
-        top3[2] = max(top3[2], min(top3[1], x));
-        top3[1] = max(top3[1], min(top3[0], x));
-        top3[0] = max(top3[0], x);
-      }
+      const uint32_t x = keys[sl];
+      top3[2] = max(top3[2], min(top3[1], x));
+      top3[1] = max(top3[1], min(top3[0], x));
+      top3[0] = max(top3[0], x);
     }
     bool exact0;
     const uint32_t t0 = kth_largest<3>(top3, 3, R, &exact0);
@@ -432,14 +434,12 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
       int ns = 0;
 #pragma unroll
       for (int sl = 0; sl < kMaxSlots; ++sl) {
-        if (sl < nslots) {
-          const bool take = keys[sl] >= t0;
-          const uint64_t mk = __ballot(take);
-          const int at = ns + __popcll(mk & lt_mask);
-          if (take && at < kSurvivors)
-            s_sel[at] = ((uint64_t)keys[sl] << 32) | (uint32_t)(64 * sl + lane);
-          ns += __popcll(mk);
-        }
+        const bool take = keys[sl] >= t0;
+        const uint64_t mk = __ballot(take);
+        const int at = ns + lanes_below(mk);
+        if (take && at < kSurvivors)
+          s_sel[at] = ((uint64_t)keys[sl] << 32) | (uint32_t)(64 * sl + lane);
+        ns += __popcll(mk);
       }
       if (ns <= 128 && R <= 128) {
         // few survivors: the register sort below orders all of them, and

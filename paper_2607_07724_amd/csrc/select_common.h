@@ -32,6 +32,16 @@ __device__ __forceinline__ uint4 pos_part(uint4 v) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// Set bits of the wave mask m held by lanes below this one (v_mbcnt: two
+// VALU operations, no mask-and-popcount per lane).
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Integer minimum (a mixed-type min() call can resolve to the floating-point
+// overload and go through double precision).
+__device__ __forceinline__ int imin(int a, int b) { return a < b ? a : b; }
+
 // fp32 score -> 32-bit key with the same order (-0 folded into +0, so equal
 // scores give equal keys); key_value inverts it.
 __device__ __forceinline__ uint32_t order_key(float f) {
@@ -77,14 +87,13 @@ __device__ __forceinline__ void select_top(const uint32_t (&key)[S], const uint3
                                            int nslots, int R, uint64_t* s_sel, int lane) {
   bool exact;
   const uint32_t thr = kth_largest<S>(key, nslots, R, &exact);
-  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   int base = 0;
 #pragma unroll
   for (int sl = 0; sl < S; ++sl) {
     if (sl < nslots) {
       const bool take = exact ? (key[sl] >= thr) : (key[sl] > thr);
       const uint64_t mk = __ballot(take);
-      if (take) s_sel[base + __popcll(mk & lt_mask)] = ((uint64_t)key[sl] << 32) | (0xffffffffu - pos[sl]);
+      if (take) s_sel[base + lanes_below(mk)] = ((uint64_t)key[sl] << 32) | (0xffffffffu - pos[sl]);
       base += __popcll(mk);
     }
   }
@@ -95,9 +104,9 @@ __device__ __forceinline__ void select_top(const uint32_t (&key)[S], const uint3
       if (sl < nslots && need > 0) {
         const bool eq = key[sl] == thr;
         const uint64_t mk = __ballot(eq);
-        const int r = __popcll(mk & lt_mask);
+        const int r = lanes_below(mk);
         if (eq && r < need) s_sel[base + r] = ((uint64_t)thr << 32) | (0xffffffffu - pos[sl]);
-        const int took = min(__popcll(mk), need);
+        const int took = imin(__popcll(mk), need);
         base += took;
         need -= took;
       }
@@ -113,7 +122,6 @@ __device__ __forceinline__ void select_top_each(const uint32_t (&key)[S], int ns
                                                 Take&& take) {
   bool exact;
   const uint32_t thr = kth_largest<S>(key, nslots, R, &exact);
-  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   int above = 0;
 #pragma unroll
   for (int sl = 0; sl < S; ++sl) {
@@ -130,8 +138,8 @@ __device__ __forceinline__ void select_top_each(const uint32_t (&key)[S], int ns
       if (sl < nslots && need > 0) {
         const bool eq = key[sl] == thr;
         const uint64_t mk = __ballot(eq);
-        if (eq && __popcll(mk & lt_mask) < need) take(sl);
-        need -= min(__popcll(mk), need);
+        if (eq && lanes_below(mk) < need) take(sl);
+        need -= imin(__popcll(mk), need);
       }
     }
   }
