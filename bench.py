@@ -34,7 +34,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default=None, choices=["C1", "C2", "C3", "C4", "C6", "P7"])
+    ap.add_argument("--workload", default=None, choices=["C1", "C2", "C3", "C4", "C6", "P7", "L8"])
     ap.add_argument("--q", type=float, default=None)
     ap.add_argument("--cpu-units", type=int, default=3072, help="oracle sample size (tile, head units)")
     ap.add_argument("--no-cpu", action="store_true")
@@ -47,7 +47,8 @@ def parse():
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the fused-selection, per-row selection and graph-replay variants")
     ap.add_argument("--no-sweep", action="store_true",
-                    help="skip the 32K-128K sweep (C2, C3, and C4 at q 0.05 / 0.25)")
+                    help="skip the 32K-256K sweep (C2, C3, C4 at q 0.05 / 0.25, and the 256K layer L8 "
+                         "with lists and fused selection)")
     ap.add_argument("--no-stack", action="store_true",
                     help="skip the 28-layer 128K stack (28/4 heads, both backbones) routed vs dense")
     ap.add_argument("--stack-steps", type=int, default=2, help="timed passes over the 28-layer stack")
@@ -291,7 +292,8 @@ def run_sweep(torch, dev, ugbs, synth, a, c4_inputs):
     stream = torch.cuda.current_stream(dev)
     cases = [(synth.WORKLOADS["C2"], None), (synth.WORKLOADS["C3"], None),
              (synth.WORKLOADS["C4"].replace(q=0.05), c4_inputs),
-             (synth.WORKLOADS["C4"].replace(q=0.25), c4_inputs)]
+             (synth.WORKLOADS["C4"].replace(q=0.25), c4_inputs),
+             (synth.WORKLOADS["L8"], None)]
     for w, given in cases:
         if given is None:
             inp = synth.generate(w, threads=16)
@@ -310,6 +312,12 @@ def run_sweep(torch, dev, ugbs, synth, a, c4_inputs):
                                         bufs.trigger.cpu().numpy(), needles)
         rec = {"workload": w.name, "seq_len": w.N, "q_heads": w.H, "kv_heads": w.Hkv, "k_budget": w.k,
                "q": w.q, "backbone": "quest" if w.backbone == 1 else "kmean", **rec}
+        if w.N > 131072:
+            # beyond 128K the selection inside the attention kernel is timed too
+            # (the regime where the paper expects the fusion to pay)
+            rec["fused_selection"] = run_fused(torch, dev, ugbs, p, Q, K, V, O, stream,
+                                               argparse.Namespace(steps=max(3, min(a.steps, 10)),
+                                                                  warmup=max(1, min(a.warmup, 3))), f_att)
         if not a.no_dense:
             dn = time_dense(torch, dev, ugbs, synth, w, Q, K, V, stream,
                             sdpa_reps=2 if w.N >= 131072 else 3, own_reps=1 if w.N >= 131072 else 2)

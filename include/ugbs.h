@@ -69,9 +69,10 @@ extern "C" {
 #define UGBS_API
 #endif
 
-#define UGBS_ABI_VERSION 7
+#define UGBS_ABI_VERSION 8
 #define UGBS_BLOCK 64          /* BLOCK_M = BLOCK_N = 64 tokens (Section 3.1, 3.2) */
-#define UGBS_MAX_BLOCKS 2048   /* N_B <= 2048, i.e. N <= 131072 */
+#define UGBS_MAX_BLOCKS 4096   /* N_B <= 4096, i.e. N <= 262144 */
+#define UGBS_MAX_BLOCKS_ROWS 2048 /* ugbs_select_rows, ugbs_bai_tiles, ugbs_bai_heads: N_B <= 2048 */
 #define UGBS_MAX_KV_WIDTH 4096 /* kv_width accepted by ugbs_attend; rho * k_budget <= 4096 */
 #define UGBS_MAX_RHO 8         /* expansion factor rho in 1..8 */
 #define UGBS_ROUTE_SCRATCH_BYTES (1u << 20) /* device scratch of ugbs_route_noalloc, per GPU */
@@ -305,7 +306,8 @@ typedef struct ugbs_bai_head {
 UGBS_API int ugbs_noise_scale(const ugbs_problem* p, const void* Q, const void* meta,
                               double* rough, float* tau, void* stream);
 
-/* Per-tile gaps and Monte Carlo identification failures.
+/* Per-tile gaps and Monte Carlo identification failures (N_B <=
+ * UGBS_MAX_BLOCKS_ROWS, else UGBS_ERR_SHAPE).
  *   scores    : [B, H, T, N_B] fp32 tile scores in the layout of
  *               ugbs_score_select's scores_out (entries of C(t) are read).
  *   tau       : [B, H] fp32 noise scale; may be NULL when n_samples == 0.
@@ -322,7 +324,8 @@ UGBS_API int ugbs_noise_scale(const ugbs_problem* p, const void* Q, const void* 
 UGBS_API int ugbs_bai_tiles(const ugbs_problem* p, const float* scores, const float* tau,
                             const float* z, int32_t n_samples, ugbs_bai_tile* tiles, void* stream);
 
-/* Per-head aggregates (ugbs_bai_head) from the tiles of ugbs_bai_tiles; q and
+/* Per-head aggregates (ugbs_bai_head) from the tiles of ugbs_bai_tiles (N_B <=
+ * UGBS_MAX_BLOCKS_ROWS, else UGBS_ERR_SHAPE); q and
  * k_budget come from p.
  *   tiles     : [B, H, T] from ugbs_bai_tiles for the same problem.
  *   tau       : [B, H] fp32, the noise scale for the closed forms.
@@ -354,7 +357,8 @@ UGBS_API int ugbs_attend_select(const ugbs_problem* p, const void* Q, const void
                                 const void* workspace, size_t workspace_bytes, void* O,
                                 void* stream);
 
-/* Per-row selection scattered into tile bitmaps (the per-row variant the
+/* Per-row selection scattered into tile bitmaps (N_B <= UGBS_MAX_BLOCKS_ROWS,
+ * else UGBS_ERR_SHAPE; the per-row variant the
  * Limitations of Section 4 name for the per-tile granularity of Section
  * 3.2).  Every query row r of tile t ranks the candidates C(t) = {1..t-1}
  * by its own score (A.2 before the max over rows: K-mean q_r . kbar_b,

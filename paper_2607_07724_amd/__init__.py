@@ -27,7 +27,8 @@ __all__ = [
 
 KMEAN, QUEST = 0, 1
 BLOCK = 64
-MAX_BLOCKS = 2048
+MAX_BLOCKS = 4096
+MAX_BLOCKS_ROWS = 2048
 MAX_KV_WIDTH = 4096
 ROUTE_SCRATCH_BYTES = 1 << 20
 _HERE = os.path.dirname(os.path.abspath(__file__))

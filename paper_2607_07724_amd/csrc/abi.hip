@@ -177,6 +177,7 @@ int ugbs_select_rows(const ugbs_problem* p, const void* Q, const void* meta, con
   Shape s;
   int st = make_shape(p, &s);
   if (st) return st;
+  if (s.NB > UGBS_MAX_BLOCKS_ROWS) return UGBS_ERR_SHAPE;
   if (!trigger || !bitmap || (!row_scores && (!Q || !meta))) return UGBS_ERR_NULL;
   if (!aligned(Q, 16) || !aligned(meta, 16) || !aligned(row_scores, 4) || !aligned(bitmap, 4))
     return UGBS_ERR_ALIGN;
@@ -220,6 +221,7 @@ int ugbs_bai_tiles(const ugbs_problem* p, const float* scores, const float* tau,
   Shape s;
   int st = make_shape(p, &s);
   if (st) return st;
+  if (s.NB > UGBS_MAX_BLOCKS_ROWS) return UGBS_ERR_SHAPE;
   if (n_samples < 0 || n_samples > (1 << 20)) return UGBS_ERR_SHAPE;
   if (!scores || !tiles || (n_samples > 0 && (!tau || !z))) return UGBS_ERR_NULL;
   if (!aligned(scores, 4) || !aligned(tau, 4) || !aligned(z, 4) || !aligned(tiles, 8))
@@ -233,6 +235,7 @@ int ugbs_bai_heads(const ugbs_problem* p, const ugbs_bai_tile* tiles, const floa
   Shape s;
   int st = make_shape(p, &s);
   if (st) return st;
+  if (s.NB > UGBS_MAX_BLOCKS_ROWS) return UGBS_ERR_SHAPE;
   if (n_samples < 0 || n_samples > (1 << 20)) return UGBS_ERR_SHAPE;
   if (!tiles || !tau || !heads) return UGBS_ERR_NULL;
   if (!aligned(tiles, 8) || !aligned(tau, 4) || !aligned(heads, 8)) return UGBS_ERR_ALIGN;

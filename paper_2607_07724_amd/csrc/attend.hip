@@ -62,8 +62,9 @@ struct AttnParams {
   int nw;
 };
 
-// Where a tile's blocks come from.
-enum Mode { kLists = 0, kSelect = 1, kBitmap = 2 };
+// Where a tile's blocks come from.  kSelectWide: kSelect for rows of more
+// than 2048 candidate blocks (64 instead of 32 candidates per lane).
+enum Mode { kLists = 0, kSelect = 1, kBitmap = 2, kSelectWide = 3 };
 
 // Waves per unit and 16-row tiles per wave: d <= 128 runs two waves of 32
 // query rows; d = 256 four waves of 16 rows (half the accumulators per wave,
@@ -196,7 +197,8 @@ attend_kernel(AttnParams P) {
       } else {
         const float* src = P.sel_scores ? P.sel_scores + rowid * s.NB + 1
                                         : P.sel_packed + packed_row(u.b * s.H + u.h, t, s.T);
-        constexpr int kSlots = UGBS_MAX_BLOCKS / 64;
+        constexpr int kSlots = MODE == kSelectWide ? UGBS_MAX_BLOCKS / 64 : 32;
+        static_assert(UGBS_MAX_BLOCKS <= 64 * 64, "at most 64 slots per lane");
         const int nslots = (nc + 63) / 64;
         uint32_t keys[kSlots];
 #pragma unroll
@@ -597,6 +599,10 @@ hipError_t launch_attend_select(const Shape& s, const uint16_t* Q, const uint16_
   P.sel_scores = scores;
   P.sel_packed = ws ? reinterpret_cast<const float*>(ws + ws_scores_off(s)) : nullptr;
   P.sel_trigger = trigger ? trigger : ws + ws_trigger_off(s);
+  if (s.NB > 32 * 64) {
+    if (s.d == 256) return launch_t<256, kSelectWide>(P, stream);
+    return s.d == 128 ? launch_t<128, kSelectWide>(P, stream) : launch_t<64, kSelectWide>(P, stream);
+  }
   if (s.d == 256) return launch_t<256, kSelect>(P, stream);
   return s.d == 128 ? launch_t<128, kSelect>(P, stream) : launch_t<64, kSelect>(P, stream);
 }

@@ -31,7 +31,7 @@ namespace ugbs {
 namespace {
 
 constexpr int kBaiUnits = 4;   // query heads of one tile per workgroup (one wave each)
-constexpr int kBaiSlots = UGBS_MAX_BLOCKS / 64;
+constexpr int kBaiSlots = UGBS_MAX_BLOCKS_ROWS / 64;
 constexpr int kHeadThreads = 256;
 
 struct TileParams {
@@ -309,9 +309,9 @@ __device__ __forceinline__ long long block_sum_i(long long x, long long* red) {
 
 __global__ void __launch_bounds__(kHeadThreads) bai_head_kernel(HeadParams P) {
 #pragma clang fp contract(off)
-  __shared__ float s_sig[UGBS_MAX_BLOCKS], s_g[UGBS_MAX_BLOCKS], s_r[UGBS_MAX_BLOCKS],
-      s_d2[UGBS_MAX_BLOCKS];
-  __shared__ int s_dk[UGBS_MAX_BLOCKS];
+  __shared__ float s_sig[UGBS_MAX_BLOCKS_ROWS], s_g[UGBS_MAX_BLOCKS_ROWS], s_r[UGBS_MAX_BLOCKS_ROWS],
+      s_d2[UGBS_MAX_BLOCKS_ROWS];
+  __shared__ int s_dk[UGBS_MAX_BLOCKS_ROWS];
   __shared__ int s_n;
   __shared__ double s_red[kHeadThreads / 64];
   __shared__ long long s_redi[kHeadThreads / 64];

@@ -85,8 +85,10 @@ __global__ void __launch_bounds__(kStatsThreads) route_stats_kernel(RouteParams 
       const uint32_t c = ans | ((1u << bit) - 1u);
       int local = 0;
       for (int t = tid; t < s.T; t += kStatsThreads) local += (s_key[t] <= c) ? 1 : 0;
-      // local is 0..2 for T <= 2048; wave-reduce with two ballots
-      const int wsum = __popcll(__ballot(local & 1)) + 2 * __popcll(__ballot(local & 2));
+      // local is 0..4 for T <= 4096 (1024 threads); wave-reduce bit by bit
+      static_assert(UGBS_MAX_BLOCKS <= 7 * kStatsThreads, "per-thread count must fit in 3 bits");
+      const int wsum = __popcll(__ballot(local & 1)) + 2 * __popcll(__ballot(local & 2)) +
+                       4 * __popcll(__ballot(local & 4));
       const int buf = bit & 1;
       if (lane == 0) s_cnt[buf][wv] = wsum;
       __syncthreads();

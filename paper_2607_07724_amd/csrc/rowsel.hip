@@ -25,7 +25,7 @@ namespace {
 
 constexpr int kRowWaves = 16;  // four per SIMD, one row each: the selection is latency-bound
 constexpr int kQuarter = 16;                 // query rows per pass
-constexpr int kRowSlots = UGBS_MAX_BLOCKS / 64;
+constexpr int kRowSlots = UGBS_MAX_BLOCKS_ROWS / 64;
 constexpr int kSurvivors = 256;               // pre-filter survivors per row
 constexpr int kMinPitch = 2 * kSurvivors;     // floats: a row's LDS region holds its survivors
 
@@ -115,7 +115,7 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
   // [16][pitch]: the quarter's scores; row r's region then holds the
   // survivors of row r (also when the scores come from memory)
   extern __shared__ __align__(16) float s_rows[];
-  __shared__ uint32_t s_bits[UGBS_MAX_BLOCKS / 32];
+  __shared__ uint32_t s_bits[UGBS_MAX_BLOCKS_ROWS / 32];
   const Shape& s = P.s;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -219,7 +219,7 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
 template <int D, bool QUEST>
 hipError_t launch_rows(RowParams P, hipStream_t stream) {
   const size_t smem = sizeof(float) * (size_t)kQuarter * P.pitch;
-  if (smem + sizeof(uint32_t) * (UGBS_MAX_BLOCKS / 32) > 65536) {
+  if (smem + sizeof(uint32_t) * (UGBS_MAX_BLOCKS_ROWS / 32) > 65536) {
     const hipError_t e = hipFuncSetAttribute((const void*)rowsel_kernel<D, QUEST>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;

@@ -355,7 +355,9 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
 
 // One wave per (b, h, t) unit, heaviest tile first; reads the unit's
 // candidate scores (packed rows of the score kernel, or a full [.., N_B] row)
-template <bool PACKED>
+// SLOTS: candidates per lane held in registers (N_B / 64 rounded up to 32 or
+// 64: rows of up to 2048 or 4096 blocks).
+template <bool PACKED, int SLOTS>
 __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
   extern __shared__ __align__(16) unsigned char smem[];
   const Shape& s = P.s;
@@ -398,7 +400,7 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
   // key (R <= 192): the R largest are among {key >= T0}, typically R plus a
   // few dozen of up to 2046.  Those survivors, in position order, go
   // through the exact selection; otherwise every candidate does.
-  constexpr int kMaxSlots = UGBS_MAX_BLOCKS / 64;
+  constexpr int kMaxSlots = SLOTS;
   const int nslots = (nc + 63) / 64;
   uint32_t keys[kMaxSlots];
   {
@@ -568,19 +570,25 @@ hipError_t launch_score(SelParams P, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <bool PACKED>
-hipError_t launch_select(const SelParams& P, hipStream_t stream) {
+template <bool PACKED, int SLOTS>
+hipError_t launch_select_s(const SelParams& P, hipStream_t stream) {
   const size_t smem = (size_t)kSelWaves * P.wave_lds;
   if (smem > 65536) {  // large budgets (k near N_B): raise the dynamic-LDS limit
-    const hipError_t e = hipFuncSetAttribute((const void*)select_kernel<PACKED>,
+    const hipError_t e = hipFuncSetAttribute((const void*)select_kernel<PACKED, SLOTS>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
   }
   const int n_units = P.s.B * P.s.H * P.s.T;
   const int n_wg = (n_units + kSelWaves - 1) / kSelWaves;
   const int grid = ((n_wg + 7) / 8) * 8;
-  select_kernel<PACKED><<<grid, 64 * kSelWaves, smem, stream>>>(P);
+  select_kernel<PACKED, SLOTS><<<grid, 64 * kSelWaves, smem, stream>>>(P);
   return hipGetLastError();
+}
+
+template <bool PACKED>
+hipError_t launch_select(const SelParams& P, hipStream_t stream) {
+  static_assert(UGBS_MAX_BLOCKS <= 64 * 64, "at most 64 slots per lane");
+  return P.s.NB <= 32 * 64 ? launch_select_s<PACKED, 32>(P, stream) : launch_select_s<PACKED, 64>(P, stream);
 }
 
 template <int OUT>

@@ -58,7 +58,7 @@ class Workload:
         return self.N // BLOCK
 
     def seed(self, layer: int = 0) -> int:
-        idx = {"C1": 1, "C2": 2, "C3": 3, "C4": 4, "C5": 5, "C6": 6}.get(self.name.split("_")[0], 9)
+        idx = {"C1": 1, "C2": 2, "C3": 3, "C4": 4, "C5": 5, "C6": 6, "L8": 8}.get(self.name.split("_")[0], 9)
         return self.base_seed + 100 * idx + layer
 
     def replace(self, **kw) -> "Workload":
@@ -85,6 +85,9 @@ WORKLOADS = {
     # 33, q 0.4, rho 2, router on the winning backbone, Quest on this model),
     # one layer at 128K
     "P7": Workload("P7", 1, 28, 4, 128, 131072, 33, 0.4, QUEST, "mixture", needles=32),
+    # the Mistral-Nemo layer at twice the longest context of the speed study
+    # (256K), where the paper expects selection fused into attention to pay
+    "L8": Workload("L8", 1, 32, 8, 128, 262144, 64, 0.1, QUEST, "mixture", needles=32),
 }
 
 

@@ -79,7 +79,7 @@ BAD = [
     (dict(block=32), "UGBS_ERR_SHAPE"),
     (dict(seq_len=1000), "UGBS_ERR_SHAPE"),
     (dict(seq_len=0), "UGBS_ERR_SHAPE"),
-    (dict(seq_len=64 * 4096), "UGBS_ERR_SHAPE"),
+    (dict(seq_len=64 * 4097), "UGBS_ERR_SHAPE"),
     (dict(rho=9), "UGBS_ERR_BUDGET"),
     (dict(rho=-1), "UGBS_ERR_BUDGET"),
     (dict(rho=8, k_budget=513), "UGBS_ERR_BUDGET"),
@@ -345,3 +345,22 @@ def test_route_noalloc_scratch_limit_and_alignment():
     odd = ctypes.c_void_p(0x100002)
     assert L.ugbs_route_noalloc(ctypes.byref(p), odd, fake, fake, None, None, None, None) == ERR_ALIGN
     assert L.ugbs_route_noalloc(ctypes.byref(p), fake, fake, fake, odd, None, None, None) == ERR_ALIGN
+
+
+def test_block_limits_per_entry_point():
+    """N_B up to 4096 (N = 262144) on the prefill path; per-row selection and
+    the Appendix D tile/head diagnostics keep N_B <= 2048."""
+    L = ugbs.lib()
+    fake = ctypes.c_void_p(0x100000)
+    SHAPE = _enum("UGBS_ERR_SHAPE")
+    assert _enum("UGBS_MAX_BLOCKS") == ugbs.MAX_BLOCKS == 4096
+    assert _enum("UGBS_MAX_BLOCKS_ROWS") == ugbs.MAX_BLOCKS_ROWS == 2048
+    p = ugbs.Problem.make(1, 8, 2, 64 * 4096, 128, 64, 0.1, ugbs.QUEST)
+    assert L.ugbs_workspace_bytes(ctypes.byref(p)) > 0
+    # valid problem: the prefill entry points fail only on the NULL pointer passed
+    assert L.ugbs_block_meta(ctypes.byref(p), None, fake, None) == _enum("UGBS_ERR_NULL")
+    assert L.ugbs_select_rows(ctypes.byref(p), fake, fake, None, fake, fake, None) == SHAPE
+    assert L.ugbs_bai_tiles(ctypes.byref(p), fake, fake, fake, 4, fake, None) == SHAPE
+    assert L.ugbs_bai_heads(ctypes.byref(p), fake, fake, 4, fake, None) == SHAPE
+    p2 = ugbs.Problem.make(1, 8, 2, 64 * 2048, 128, 64, 0.1, ugbs.QUEST)
+    assert L.ugbs_select_rows(ctypes.byref(p2), None, None, None, fake, fake, None) == _enum("UGBS_ERR_NULL")

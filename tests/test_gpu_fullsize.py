@@ -180,7 +180,7 @@ def check_all(r):
     print(f"{w.name}: {len(units)} sampled units, near-tie exemptions {exempt}")
 
 
-@pytest.mark.parametrize("name", ["C2", "C3", "C4", "C6", "P7"])
+@pytest.mark.parametrize("name", ["C2", "C3", "C4", "C6", "P7", "L8"])
 def test_full_size_workload(name):
     r = run_full(synth.WORKLOADS[name])
     check_all(r)

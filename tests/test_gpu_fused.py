@@ -177,10 +177,11 @@ def test_tiny_sequences(N):
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name", ["C2", "C4"])
+@pytest.mark.parametrize("name", ["C2", "C4", "L8"])
 def test_full_size_fused_equals_lists(name):
-    """32K and 128K layers in the benchmark's configuration: the fused layer's
-    output, sigma and trigger flags equal the lists layer's bit for bit."""
+    """32K, 128K and 256K layers in the benchmark's configuration: the fused
+    layer's output, sigma and trigger flags equal the lists layer's bit for
+    bit (at 256K the fused kernel holds 64 candidates per lane)."""
     w = synth.WORKLOADS[name]
     inp = synth.generate(w, threads=16)
     a, b = _layers(w, inp)

@@ -1,5 +1,6 @@
-"""GPU parity at the largest sizes the ABI accepts: N_B = 2048 blocks (N =
-131072) and kv_idx rows of up to 4096 slots (rho k = UGBS_MAX_KV_WIDTH).
+"""GPU parity at the largest sizes the ABI accepts: N_B = 4096 blocks (N =
+262144; and 2048, the largest that keeps 32 candidates per lane) and kv_idx
+rows of up to 4096 slots (rho k = UGBS_MAX_KV_WIDTH).
 
 Selection on given tile scores and the route are compared with the oracle
 bit for bit; the budgets reach R = rho k - |F| far above the 128 winners
@@ -33,23 +34,25 @@ def _need_gpu():
 _scores = {}
 
 
-def scores():
+def scores(nb=NB):
     """[B, H, T, N_B] fp32 tile scores with heavy ties and signed zeros on
     one head and distinct values on the other."""
-    if "S" not in _scores:
-        g = np.random.default_rng(2048)
-        S = np.empty((B, H, NB, NB), np.float32)
-        S[0, 0] = np.round(g.standard_normal((NB, NB)) * 3.0)   # small integers: many ties
-        S[0, 0][g.random((NB, NB)) < 0.05] = -0.0
-        S[0, 1] = g.standard_normal((NB, NB)).astype(np.float32)
-        _scores["S"] = S
-    return _scores["S"]
+    if nb not in _scores:
+        g = np.random.default_rng(2048 + nb)
+        S = np.empty((B, H, nb, nb), np.float32)
+        S[0, 0] = np.round(g.standard_normal((nb, nb)) * 3.0)   # small integers: many ties
+        S[0, 0][g.random((nb, nb)) < 0.05] = -0.0
+        S[0, 1] = g.standard_normal((nb, nb)).astype(np.float32)
+        _scores[nb] = S
+    return _scores[nb]
 
 
-@pytest.mark.parametrize("k,rho", [(3, 2), (700, 2), (1024, 2), (2048, 2), (512, 8), (1365, 3), (4096, 1)])
-def test_selection_and_route_at_maximum_width(k, rho):
+@pytest.mark.parametrize("nb", [2048, 4096])
+@pytest.mark.parametrize("k,rho", [(3, 2), (64, 2), (700, 2), (1024, 2), (2048, 2), (512, 8), (1365, 3), (4096, 1)])
+def test_selection_and_route_at_maximum_width(k, rho, nb):
     torch = __import__("torch")
-    S = scores()
+    N, NB = 64 * nb, nb
+    S = scores(nb)
     p = ugbs.Problem.make(B, H, HKV, N, D, k, 0.1, synth.KMEAN, rho=rho)
     assert p.W == rho * k <= ugbs.MAX_KV_WIDTH
     Q = torch.zeros((B, H, N, D), dtype=torch.bfloat16, device="cuda")
