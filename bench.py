@@ -251,7 +251,7 @@ def time_dense(torch, dev, ugbs, synth, w, Q, K, V, stream, sdpa_reps=3, own_rep
     except Exception as ex:  # keep the routed figures even if SDPA is unavailable
         log(f"torch SDPA failed: {ex!r}")
     kvd = torch.from_numpy(synth.dense_kv_idx(w.B, w.H, w.T)).to(dev)
-    pd = ugbs.Problem.make(w.B, w.H, w.Hkv, w.N, w.d, w.NB, 0.0, w.backbone)
+    pd = ugbs.Problem.make(w.B, w.H, w.Hkv, w.N, w.d, w.NB, 0.0, w.backbone, rho=1)   # every block: W = N_B
     Od = torch.empty_like(Q)
     ugbs.ugbs_attend(pd, Q, K, V, kvd, Od)
     torch.cuda.synchronize(dev)
@@ -858,7 +858,7 @@ def run_stack(torch, dev, ugbs, synth, steps):
     except Exception as ex:
         log(f"stack SDPA failed: {ex!r}")
     kvd = torch.from_numpy(synth.dense_kv_idx(w0.B, w0.H, w0.T)).to(dev)
-    pd = ugbs.Problem.make(w0.B, w0.H, w0.Hkv, w0.N, w0.d, w0.NB, 0.0, w0.backbone)
+    pd = ugbs.Problem.make(w0.B, w0.H, w0.Hkv, w0.N, w0.d, w0.NB, 0.0, w0.backbone, rho=1)
     e0.record(stream)
     for Q, K, V in layers:
         ugbs.ugbs_attend(pd, Q, K, V, kvd, O)
