@@ -626,7 +626,7 @@ def run_bai(a, torch, dev, ugbs, synth, w):
     Q, K = to_dev(inp.Q), to_dev(inp.K)
     p = ugbs.Problem.make(w.B, w.H, w.Hkv, w.N, w.d, w.k, w.q, w.backbone)
     B, H, T, NB = w.B, w.H, w.T, w.NB
-    meta = torch.empty((B, w.Hkv, NB, p.meta_width, w.d), dtype=torch.bfloat16, device=dev)
+    meta = torch.empty((B, w.Hkv, NB, w.d, p.meta_width), dtype=torch.bfloat16, device=dev)
     idx = torch.empty((B, H, T, p.W), dtype=torch.int32, device=dev)
     sig = torch.empty((B, H, T), dtype=torch.float32, device=dev)
     scores = torch.empty((B, H, T, NB), dtype=torch.float32, device=dev)

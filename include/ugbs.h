@@ -69,7 +69,7 @@ extern "C" {
 #define UGBS_API
 #endif
 
-#define UGBS_ABI_VERSION 8
+#define UGBS_ABI_VERSION 9
 #define UGBS_BLOCK 64          /* BLOCK_M = BLOCK_N = 64 tokens (Section 3.1, 3.2) */
 #define UGBS_MAX_BLOCKS 4096   /* N_B <= 4096, i.e. N <= 262144 */
 #define UGBS_MAX_BLOCKS_ROWS 2048 /* ugbs_select_rows, ugbs_bai_tiles, ugbs_bai_heads: N_B <= 2048 */
@@ -127,8 +127,10 @@ typedef struct ugbs_problem {
  *          fits in 53 bits).  Beyond that range the sum may round in its
  *          last fp64 bit, which changes the bf16 mean only when it lies
  *          within that rounding of a bf16 rounding boundary.
- *          UGBS_QUEST: [B, H_kv, N_B, 2, d] bf16, element-wise minimum then
- *          element-wise maximum over the block's 64 keys.
+ *          UGBS_QUEST: [B, H_kv, N_B, d, 2] bf16: for every channel the
+ *          pair (element-wise minimum, element-wise maximum) over the
+ *          block's 64 keys, adjacent (the order in which the scoring
+ *          kernel's 2:4-sparse contraction reads them).
  *          16-byte aligned.  A zero is always written as +0. */
 UGBS_API int ugbs_block_meta(const ugbs_problem* p, const void* K, void* meta, void* stream);
 

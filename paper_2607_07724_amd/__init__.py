@@ -177,11 +177,12 @@ def _raise(fn, st):
 
 
 def ugbs_block_meta(p: Problem, K, meta, stream=None):
-    """Stage 1 (A.1): K [B,Hkv,N,d] bf16 -> meta [B,Hkv,N_B,(1|2),d] bf16."""
+    """Stage 1 (A.1): K [B,Hkv,N,d] bf16 -> meta [B,Hkv,N_B,d,(1|2)] bf16
+    (Quest: per channel the pair (min, max))."""
     bf = _bf16()
     dev = K.device
     k = _check("K", K, (p.batch, p.n_kv_heads, p.seq_len, p.head_dim), bf)
-    m = _check("meta", meta, (p.batch, p.n_kv_heads, p.NB, p.meta_width, p.head_dim), bf, dev)
+    m = _check("meta", meta, (p.batch, p.n_kv_heads, p.NB, p.head_dim, p.meta_width), bf, dev)
     _raise("ugbs_block_meta", lib().ugbs_block_meta(ctypes.byref(p), k, m, _stream(stream)))
 
 
@@ -194,7 +195,7 @@ def ugbs_score_select(p: Problem, Q, meta, idx_sorted, sigma, scores_in=None, sc
     bf = _bf16()
     dev = Q.device
     q = _check("Q", Q, (p.batch, p.n_heads, p.seq_len, p.head_dim), bf)
-    m = _check("meta", meta, (p.batch, p.n_kv_heads, p.NB, p.meta_width, p.head_dim), bf, dev)
+    m = _check("meta", meta, (p.batch, p.n_kv_heads, p.NB, p.head_dim, p.meta_width), bf, dev)
     si = _opt("scores_in", scores_in, (p.batch, p.n_heads, p.T, p.NB), (torch.float32,), dev)
     so = _opt("scores_out", scores_out, (p.batch, p.n_heads, p.T, p.NB), (torch.float32,), dev)
     ix = _opt("idx_sorted", idx_sorted, (p.batch, p.n_heads, p.T, p.W), (torch.int32,), dev)
@@ -302,7 +303,7 @@ def ugbs_select_rows(p: Problem, trigger, bitmap, Q=None, meta=None, row_scores=
     tr = _check("trigger", trigger, (p.batch, p.T), (torch.uint8,), dev)
     bm = _check("bitmap", bitmap, (p.batch, p.n_heads, p.T, bitmap_words(p)), (torch.int32,), dev)
     q = _opt("Q", Q, (p.batch, p.n_heads, p.seq_len, p.head_dim), bf, dev)
-    m = _opt("meta", meta, (p.batch, p.n_kv_heads, p.NB, p.meta_width, p.head_dim), bf, dev)
+    m = _opt("meta", meta, (p.batch, p.n_kv_heads, p.NB, p.head_dim, p.meta_width), bf, dev)
     rs = _opt("row_scores", row_scores, (p.batch, p.n_heads, p.seq_len, p.NB), (torch.float32,), dev)
     _raise("ugbs_select_rows", lib().ugbs_select_rows(ctypes.byref(p), q, m, rs, tr, bm, _stream(stream)))
 
@@ -363,7 +364,7 @@ def ugbs_noise_scale(p: Problem, Q, meta, rough, tau, stream=None):
     bf = _bf16()
     dev = Q.device
     q = _check("Q", Q, (p.batch, p.n_heads, p.seq_len, p.head_dim), bf)
-    m = _check("meta", meta, (p.batch, p.n_kv_heads, p.NB, p.meta_width, p.head_dim), bf, dev)
+    m = _check("meta", meta, (p.batch, p.n_kv_heads, p.NB, p.head_dim, p.meta_width), bf, dev)
     r = _check("rough", rough, (p.batch, p.n_heads, p.T), (torch.float64,), dev)
     ta = _check("tau", tau, (p.batch, p.n_heads), (torch.float32,), dev)
     _raise("ugbs_noise_scale", lib().ugbs_noise_scale(ctypes.byref(p), q, m, r, ta, _stream(stream)))
@@ -404,7 +405,7 @@ class Buffers:
     def __init__(self, p: Problem, device="cuda"):
         import torch
         B, H, Hkv, T, NB, d = p.batch, p.n_heads, p.n_kv_heads, p.T, p.NB, p.head_dim
-        self.meta = torch.empty((B, Hkv, NB, p.meta_width, d), dtype=torch.bfloat16, device=device)
+        self.meta = torch.empty((B, Hkv, NB, d, p.meta_width), dtype=torch.bfloat16, device=device)
         self.idx_sorted = torch.empty((B, H, T, p.W), dtype=torch.int32, device=device)
         self.sigma = torch.empty((B, H, T), dtype=torch.float32, device=device)
         self.kv_idx = torch.empty((B, H, T, p.W), dtype=torch.int32, device=device)

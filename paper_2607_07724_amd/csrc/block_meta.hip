@@ -6,7 +6,8 @@
 // consecutive lanes cover a key row, so each row is one contiguous segment.
 // The parts are combined across lanes (XOR shuffles).  K is streamed exactly
 // once: the kernel is HBM-bound (algorithmic bytes per block: 64*d*2 read +
-// c*d*2 written, c = 1 K-mean, 2 Quest).
+// c*d*2 written, c = 1 K-mean, 2 Quest).  Quest rows hold, per channel, the
+// pair (minimum, maximum) adjacently.
 //
 // K-mean: the 64 values of a channel are summed in fp64 (every partial sum
 // is exact when the nonzero values' binary exponents lie within 39 of each
@@ -130,15 +131,14 @@ __global__ void __launch_bounds__(256) block_meta_kernel(const uint16_t* __restr
         hi[e] = b > hi[e] ? b : hi[e];
       }
     if (part == 0) {
-      uint32_t omin[4], omax[4];
+      // channel pairs (min, max) adjacent: the lane's 8 channels are 32
+      // contiguous bytes of the block's 2 d-long row
+      uint32_t pr[8];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        omin[e] = exact_bf16_bits(lo[2 * e]) | (exact_bf16_bits(lo[2 * e + 1]) << 16);
-        omax[e] = exact_bf16_bits(hi[2 * e]) | (exact_bf16_bits(hi[2 * e + 1]) << 16);
-      }
-      uint16_t* row = meta + (size_t)bh_blk * 2 * D + cg * 8;
-      *reinterpret_cast<uint4*>(row) = make_uint4(omin[0], omin[1], omin[2], omin[3]);
-      *reinterpret_cast<uint4*>(row + D) = make_uint4(omax[0], omax[1], omax[2], omax[3]);
+      for (int e = 0; e < 8; ++e) pr[e] = exact_bf16_bits(lo[e]) | (exact_bf16_bits(hi[e]) << 16);
+      uint16_t* row = meta + (size_t)bh_blk * 2 * D + 2 * cg * 8;
+      *reinterpret_cast<uint4*>(row) = make_uint4(pr[0], pr[1], pr[2], pr[3]);
+      *reinterpret_cast<uint4*>(row + 8) = make_uint4(pr[4], pr[5], pr[6], pr[7]);
     }
   }
 }

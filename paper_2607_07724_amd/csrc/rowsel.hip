@@ -11,8 +11,8 @@
 //   scores     wave w computes the 16 x 16 score blocks of chunks w, w + 16,
 //              ... on bf16 MFMA (the 16 query rows in registers as the A
 //              operand, the chunk's metadata rows straight from L2 as the B
-//              operand; Quest as the exact split [q- | q+] . [kmin; kmax],
-//              split per MFMA at d = 256) into an LDS array [16 rows x N_B];
+//              operand; Quest as the 2:4-sparse contraction of quest_index
+//              on v_smfmac) into an LDS array [16 rows x N_B];
 //   selection  wave w takes row w: keys, the top-3 pre-filter and the radix
 //              threshold of the selection kernel (the survivors staged in
 //              the row's own LDS space once its keys are in registers), and
@@ -110,8 +110,7 @@ __device__ __forceinline__ void row_top(const float* row, int nc, int R, int lan
 template <int D, bool QUEST>
 __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
   constexpr int KD = QUEST ? 2 * D : D;        // metadata row length
-  constexpr bool FLY = QUEST && D >= 256;      // split per MFMA (register budget)
-  constexpr int KS = FLY ? D / 32 : KD / 32;   // A registers per lane
+  constexpr int KS = D / 32;                   // k-steps of 32 channels (raw query rows)
   // [16][pitch]: the quarter's scores; row r's region then holds the
   // survivors of row r (also when the scores come from memory)
   extern __shared__ __align__(16) float s_rows[];
@@ -155,24 +154,24 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
       } else {
         // ---- scores of rows 16 qr .. 16 qr + 15, chunk by chunk ----------
         bf16x8 a[KS];
+        uint32_t qidx[QUEST ? KS : 1];
         const uint16_t* qrow = qtile + (size_t)(kQuarter * qr + c16) * D;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          if constexpr (QUEST && !FLY) {
-            const uint4 v = *reinterpret_cast<const uint4*>(qrow + (ks % (D / 32)) * 32 + 8 * g);
-            a[ks] = as_bf16x8(ks < D / 32 ? neg_part(v) : pos_part(v));
-          } else {
-            a[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g));
-          }
+          const uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g);
+          a[ks] = as_bf16x8(v);
+          if constexpr (QUEST) qidx[ks] = quest_index(v);
         }
-        // the chunk's metadata rows straight from L2 as the B operand
-        constexpr int KB = FLY ? 2 * KS : KS;
+        // the chunk's metadata rows straight from L2 as the B operand; Quest:
+        // per k-step the (kmin, kmax) pairs of channels 32 ks + 4 g .. + 3 and
+        // 32 ks + 16 + 4 g .. + 3 (see quest_index)
+        constexpr int KB = QUEST ? 2 * KS : KS;
         auto load_b = [&](int c, uint4 (&bv)[KB]) {
           const int p = 16 * c + c16;  // block 1 + p; past the last candidate block 1 is read
-          const uint16_t* mrow = mhead + (size_t)(1 + (p < nc ? p : 0)) * KD + 8 * g;
+          const uint16_t* mrow = mhead + (size_t)(1 + (p < nc ? p : 0)) * KD;
 #pragma unroll
           for (int j = 0; j < KB; ++j) {
-            const int off = FLY ? (j % KS) * 32 + (j / KS) * D : 32 * j;   // FLY: kmin k-steps, then kmax
+            const int off = QUEST ? 64 * (j / 2) + 32 * (j % 2) + 8 * g : 32 * j + 8 * g;
             bv[j] = *reinterpret_cast<const uint4*>(mrow + off);
           }
         };
@@ -181,14 +180,11 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
           load_b(c, cur);
           const int p = 16 * c + c16;
           f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-          if constexpr (FLY) {
+          if constexpr (QUEST) {
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-              const uint4 raw = __builtin_bit_cast(uint4, a[ks]);
-              acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(neg_part(raw)), as_bf16x8(cur[ks]), acc, 0, 0, 0);
-              acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(pos_part(raw)), as_bf16x8(cur[KS + ks]), acc,
-                                                            0, 0, 0);
-            }
+            for (int ks = 0; ks < KS; ++ks)
+              acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[ks], as_bf16x16(cur[2 * ks], cur[2 * ks + 1]), acc,
+                                                              (int)qidx[ks], 0, 0);
           } else {
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks)

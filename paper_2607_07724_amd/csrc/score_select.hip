@@ -4,15 +4,16 @@
 // score_kernel: one workgroup per 4 consecutive (Q-tile, query head) units
 // of one (batch, kv head), sibling heads of one tile or of two adjacent
 // tiles (see Group); each wave owns one unit (64 rows of its tile).
-// Scoring is a dense contraction on bf16 MFMA
-// (v_mfma_f32_16x16x32_bf16):
-//   S[64 rows x 16 blocks] = Qx[64 x KD] * Mx[KD x 16 blocks]
-// with, for K-mean, Qx = Q and Mx = kbar (KD = d), and for Quest the exact
-// split form of Eq. (quest-score): for kmax >= kmin,
-//   max(q kmax, q kmin) = min(q,0) kmin + max(q,0) kmax,
-// so Qx = [q- | q+] and Mx = [kmin | kmax] (KD = 2d, the metadata row as
-// stored).  Every product is an exact bf16 x bf16 product; sums are fp32.
-// The wave's 64-row Qx tile stays in registers as the A operand.  Metadata
+// Scoring is a contraction on the matrix cores:
+//   S[64 rows x 16 blocks] = Q[64 x d] * M[d x 16 blocks]
+// K-mean: M = kbar, dense bf16 MFMA (v_mfma_f32_16x16x32_bf16).  Quest: the
+// bound of Eq. (quest-score), sum_c q_c (q_c > 0 ? kmax_c : kmin_c), as a
+// 2:4-sparse contraction (v_smfmac_f32_16x16x64_bf16, twice the dense rate):
+// the uncompressed operand interleaves (kmin_c, kmax_c), which is how the
+// metadata rows are stored, the raw query values are the compressed operand
+// and their signs the sparsity indices (quest_index).  Every product is an
+// exact bf16 x bf16 product; sums are fp32.  The wave's 64 raw query rows
+// stay in registers as the A operand (with the indices for Quest).  Metadata
 // rows (the B operand) come in chunks of 16 or 32 blocks that the workgroup's
 // waves fetch together with direct-to-LDS loads into a 4-slot ring (three
 // chunks in flight), so each chunk crosses L2 once per workgroup; in LDS
@@ -224,27 +225,21 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
                       : (ROUGH ? nullptr : P.scores_out + row * s.NB + 1);
   double rough = 0.0;
   if (nc_top > 0) {
-    // ---- A operand: this wave's 64 query rows (Quest: [q- | q+]) ----------
-    // d = 256 Quest: the split pair would take 256 registers per lane, so the
-    // raw q rows stay in registers and are split per MFMA (two bit masks)
-    constexpr bool FLY = QUEST && D >= 256;
-    constexpr int KA = FLY ? D / 32 : KS;
+    // ---- A operand: this wave's 64 query rows, raw, for both backbones;
+    // Quest adds the 2:4 sparsity indices that select kmax or kmin per
+    // channel by the sign of q (see quest_index)
+    constexpr int KA = D / 32;
     bf16x8 a[4][KA];
+    uint32_t qidx[4][QUEST ? KA : 1];
     const uint16_t* qtile = P.Q + (((size_t)gr.b * s.H + h) * s.N + (size_t)t * kBlock) * D;
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) {
       const uint16_t* qrow = qtile + (size_t)(16 * rt + c16) * D;
 #pragma unroll
       for (int ks = 0; ks < KA; ++ks) {
-        if constexpr (FLY) {
-          a[rt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g));
-        } else if constexpr (QUEST) {
-          const int kk = (ks % (D / 32)) * 32 + 8 * g;
-          const uint4 v = *reinterpret_cast<const uint4*>(qrow + kk);
-          a[rt][ks] = as_bf16x8(ks < D / 32 ? neg_part(v) : pos_part(v));
-        } else {
-          a[rt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g));
-        }
+        const uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g);
+        a[rt][ks] = as_bf16x8(v);
+        if constexpr (QUEST) qidx[rt][ks] = quest_index(v);
       }
     }
     __builtin_amdgcn_s_waitcnt(0x70 | 0xf00);  // vmcnt(0): Q is in registers
@@ -294,19 +289,18 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
           f32x4 acc[4];
 #pragma unroll
           for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if constexpr (FLY) {
-            // min(q,0) . kmin + max(q,0) . kmax, k-step by k-step
+          if constexpr (QUEST) {
+            // sum over the k-step's 32 channels of q * (q > 0 ? kmax : kmin):
+            // B holds the (kmin, kmax) pairs of channels 4 g .. 4 g + 3 and
+            // 16 + 4 g .. 16 + 4 g + 3 (two 16-byte columns of the row)
 #pragma unroll
             for (int ks = 0; ks < KA; ++ks) {
-              const bf16x8 bmin = as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(br, 4 * ks + g)));
-              const bf16x8 bmax =
-                  as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(br, 4 * (ks + D / 32) + g)));
+              const uint4 b0 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + g));
+              const uint4 b1 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + 4 + g));
+              const bf16x16 b = as_bf16x16(b0, b1);
 #pragma unroll
-              for (int rt = 0; rt < 4; ++rt) {
-                const uint4 raw = __builtin_bit_cast(uint4, a[rt][ks]);
-                acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(neg_part(raw)), bmin, acc[rt], 0, 0, 0);
-                acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(pos_part(raw)), bmax, acc[rt], 0, 0, 0);
-              }
+              for (int rt = 0; rt < 4; ++rt)
+                acc[rt] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[rt][ks], b, acc[rt], (int)qidx[rt][ks], 0, 0);
             }
           } else {
 #pragma unroll

@@ -32,6 +32,38 @@ __device__ __forceinline__ uint4 pos_part(uint4 v) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+typedef __attribute__((__vector_size__(16 * sizeof(__bf16)))) __bf16 bf16x16;
+struct U4Pair {
+  uint4 lo, hi;
+};
+__device__ __forceinline__ bf16x16 as_bf16x16(uint4 lo, uint4 hi) {
+  return __builtin_bit_cast(bf16x16, (U4Pair{lo, hi}));
+}
+
+// The Quest bound of Eq. (quest-score) as a 2:4-sparse contraction.  For
+// each channel c, max(q_c kmax_c, q_c kmin_c) = q_c * (q_c > 0 ? kmax_c :
+// kmin_c).  With the uncompressed operand ordered k = 2 c + {0: kmin, 1:
+// kmax}, every group of four k (channels 2i, 2i + 1) holds exactly two
+// selected entries, so v_smfmac_f32_16x16x64_bf16 computes the bound of 32
+// channels per k-step with the raw query values as its compressed A operand
+// (lane group g of a k-step holds channels 8 g .. 8 g + 7, element e being
+// channel 8 g + e, the second of its group when e is odd) and these indices:
+// element e sits at position 2 (e mod 2) + [q > 0] of its group, two bits
+// per element, element 0 lowest.  q = +0 or -0 selects kmin (a zero
+// product either way).
+__device__ __forceinline__ uint32_t quest_index(uint4 v) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  uint32_t idx = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t lo = w[i] & 0xffffu, hi = w[i] >> 16;
+    const uint32_t plo = (lo != 0u && !(lo & 0x8000u)) ? 1u : 0u;
+    const uint32_t phi = 2u + ((hi != 0u && !(hi & 0x8000u)) ? 1u : 0u);
+    idx |= (plo << (4 * i)) | (phi << (4 * i + 2));
+  }
+  return idx;
+}
+
 // Set bits of the wave mask m held by lanes below this one (v_mbcnt: two
 // VALU operations, no mask-and-popcount per lane).
 __device__ __forceinline__ int lanes_below(uint64_t m) {

@@ -27,6 +27,22 @@ def host(x) -> np.ndarray:
     return x.cpu().numpy()
 
 
+def meta_to_gpu(m: np.ndarray) -> np.ndarray:
+    """The oracle's block metadata [.., w, d] (K-mean w = 1; Quest rows min,
+    max) in the library's layout [.., d, w] (Quest: per channel the pair
+    (min, max)); a relayout only, no arithmetic."""
+    return np.ascontiguousarray(np.swapaxes(m, -1, -2))
+
+
+def meta_from_gpu(m: np.ndarray) -> np.ndarray:
+    """The library's metadata [.., d, w] in the oracle's layout [.., w, d]."""
+    return np.ascontiguousarray(np.swapaxes(m, -1, -2))
+
+
+def dev_meta(m: np.ndarray):
+    return dev_bf16(meta_to_gpu(m))
+
+
 def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
     return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 

@@ -26,7 +26,7 @@ from oracle import bai
 import paper_2607_07724_amd as ugbs
 from paper_2607_07724_amd import synth
 
-from gpu_helpers import dev, dev_bf16, host
+from gpu_helpers import dev, dev_bf16, dev_meta, host
 
 pytestmark = pytest.mark.gpu
 
@@ -242,7 +242,7 @@ def gpu_noise(p, Q, meta_np):
     torch = __import__("torch")
     rough = torch.empty((p.batch, p.n_heads, p.T), dtype=torch.float64, device="cuda")
     tau = torch.empty((p.batch, p.n_heads), dtype=torch.float32, device="cuda")
-    ugbs.ugbs_noise_scale(p, Q, dev_bf16(meta_np), rough, tau)
+    ugbs.ugbs_noise_scale(p, Q, dev_meta(meta_np), rough, tau)
     torch.cuda.synchronize()
     return host(rough), host(tau)
 
@@ -319,7 +319,7 @@ def test_chain_on_scores_out_matches_selection_sigma(name):
     w = c["w"]
     p = problem(w)
     Q = dev_bf16(c["inp"].Q)
-    meta = dev_bf16(c["meta"])
+    meta = dev_meta(c["meta"])
     idx = torch.empty((w.B, w.H, w.T, p.W), dtype=torch.int32, device="cuda")
     sig = torch.empty((w.B, w.H, w.T), dtype=torch.float32, device="cuda")
     so = torch.empty((w.B, w.H, w.T, w.NB), dtype=torch.float32, device="cuda")
@@ -358,7 +358,7 @@ def test_full_size_diagnostics(name):
     p = problem(w)
     B, H, T, NB = w.B, w.H, w.T, w.NB
     Q, K = dev_bf16(inp.Q), dev_bf16(inp.K)
-    meta = torch.empty((B, w.Hkv, NB, p.meta_width, w.d), dtype=torch.bfloat16, device="cuda")
+    meta = torch.empty((B, w.Hkv, NB, w.d, p.meta_width), dtype=torch.bfloat16, device="cuda")
     ugbs.ugbs_block_meta(p, K, meta)
     idx = torch.empty((B, H, T, p.W), dtype=torch.int32, device="cuda")
     sig = torch.empty((B, H, T), dtype=torch.float32, device="cuda")

@@ -22,7 +22,8 @@ import oracle
 import paper_2607_07724_amd as ugbs
 from paper_2607_07724_amd import synth
 
-from gpu_helpers import attention_error, bf16_to_f64, dev, dev_bf16, host, host_bits, near_tie_ok
+from gpu_helpers import (attention_error, bf16_to_f64, dev, dev_bf16, host, host_bits,
+                         meta_from_gpu, near_tie_ok)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 ATOL_MAX, ATOL_RMS = 2e-2, 2e-3
@@ -83,7 +84,7 @@ def check_all(r):
     NB, k, T = w.NB, w.k, w.T
     # ---- metadata: every block, bit-exact
     meta = oracle.block_meta(w.backbone, inp.K, nthreads=16)
-    assert np.array_equal(host_bits(bufs.meta).reshape(meta.shape), meta)
+    assert np.array_equal(meta_from_gpu(host_bits(bufs.meta)), meta)
 
     # ---- tile scores of sampled units: fp32 accumulation bound
     S = oracle.tile_scores(w.backbone, inp.Q, meta, w.Hkv, units=units, nthreads=16)

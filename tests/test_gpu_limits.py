@@ -56,7 +56,7 @@ def test_selection_and_route_at_maximum_width(k, rho, nb):
     p = ugbs.Problem.make(B, H, HKV, N, D, k, 0.1, synth.KMEAN, rho=rho)
     assert p.W == rho * k <= ugbs.MAX_KV_WIDTH
     Q = torch.zeros((B, H, N, D), dtype=torch.bfloat16, device="cuda")
-    meta = torch.zeros((B, HKV, NB, 1, D), dtype=torch.bfloat16, device="cuda")
+    meta = torch.zeros((B, HKV, NB, D, 1), dtype=torch.bfloat16, device="cuda")
     idx = torch.empty((B, H, NB, p.W), dtype=torch.int32, device="cuda")
     sig = torch.empty((B, H, NB), dtype=torch.float32, device="cuda")
     ugbs.ugbs_score_select(p, Q, meta, idx, sig, scores_in=dev(S))

@@ -23,8 +23,8 @@ import oracle
 import paper_2607_07724_amd as ugbs
 from paper_2607_07724_amd import synth
 
-from gpu_helpers import (attention_error, bf16_to_f64, dev, dev_bf16, host, host_bits,
-                         near_tie_ok)
+from gpu_helpers import (attention_error, bf16_to_f64, dev, dev_bf16, dev_meta, host, host_bits,
+                         meta_from_gpu, near_tie_ok)
 
 pytestmark = pytest.mark.gpu
 ATOL_MAX, ATOL_RMS = 2e-2, 2e-3
@@ -97,18 +97,18 @@ def test_block_meta_bit_exact(name, backbone):
     p = problem(w)
     torch = __import__("torch")
     K = dev_bf16(c["inp"].K)
-    meta = torch.empty((w.B, w.Hkv, w.NB, p.meta_width, w.d), dtype=torch.bfloat16, device="cuda")
+    meta = torch.empty((w.B, w.Hkv, w.NB, w.d, p.meta_width), dtype=torch.bfloat16, device="cuda")
     ugbs.ugbs_block_meta(p, K, meta)
     torch.cuda.synchronize()
     ref = oracle.block_meta(backbone, c["inp"].K)
-    assert np.array_equal(host_bits(meta), ref)
+    assert np.array_equal(meta_from_gpu(host_bits(meta)), ref)
 
 
 # ---------------------------------------------------------------- stages 2-3
 
 def _select_gpu(w, p, Q, meta_np, scores_in=None, want_scores=False):
     torch = __import__("torch")
-    meta = dev_bf16(meta_np)
+    meta = dev_meta(meta_np)
     idx = torch.empty((w.B, w.H, w.T, p.W), dtype=torch.int32, device="cuda")
     sig = torch.empty((w.B, w.H, w.T), dtype=torch.float32, device="cuda")
     so = torch.empty((w.B, w.H, w.T, w.NB), dtype=torch.float32, device="cuda") if want_scores else None
@@ -315,7 +315,7 @@ def test_end_to_end_against_oracle(name):
     c = case(name)
     w, inp = c["w"], c["inp"]
     g = _pipeline_gpu(w, inp)
-    assert np.array_equal(g["meta"].reshape(c["meta"].shape), c["meta"])
+    assert np.array_equal(meta_from_gpu(g["meta"]), c["meta"])
     NB, k = w.NB, w.k
     exempt = 0
     rows_equal = np.ones((w.B, w.H, w.T), bool)

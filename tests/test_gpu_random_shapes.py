@@ -22,7 +22,7 @@ import oracle
 import paper_2607_07724_amd as ugbs
 from paper_2607_07724_amd import synth
 
-from gpu_helpers import attention_error, dev, dev_bf16, host, host_bits, near_tie_ok
+from gpu_helpers import attention_error, dev, dev_bf16, dev_meta, host, host_bits, meta_from_gpu, near_tie_ok
 
 pytestmark = pytest.mark.gpu
 ATOL_MAX, ATOL_RMS = 2e-2, 2e-3
@@ -76,15 +76,15 @@ def test_random_shape_against_oracle(seed):
     Q, K, V = dev_bf16(inp.Q), dev_bf16(inp.K), dev_bf16(inp.V)
 
     # metadata, bit-exact
-    gmeta = torch.empty((w.B, w.Hkv, w.NB, p.meta_width, w.d), dtype=torch.bfloat16, device="cuda")
+    gmeta = torch.empty((w.B, w.Hkv, w.NB, w.d, p.meta_width), dtype=torch.bfloat16, device="cuda")
     ugbs.ugbs_block_meta(p, K, gmeta)
     torch.cuda.synchronize()
-    assert np.array_equal(host_bits(gmeta), meta)
+    assert np.array_equal(meta_from_gpu(host_bits(gmeta)), meta)
 
     # selection on the oracle's tile scores, bit-exact
     gidx = torch.empty((w.B, w.H, w.T, p.W), dtype=torch.int32, device="cuda")
     gsig = torch.empty((w.B, w.H, w.T), dtype=torch.float32, device="cuda")
-    ugbs.ugbs_score_select(p, Q, dev_bf16(meta), gidx, gsig, scores_in=dev(S))
+    ugbs.ugbs_score_select(p, Q, dev_meta(meta), gidx, gsig, scores_in=dev(S))
     torch.cuda.synchronize()
     assert np.array_equal(host(gidx), idx)
     assert np.array_equal(host(gsig).view(np.uint32), sig.view(np.uint32))

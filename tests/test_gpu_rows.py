@@ -20,7 +20,7 @@ import oracle
 import paper_2607_07724_amd as ugbs
 from paper_2607_07724_amd import synth
 
-from gpu_helpers import attention_error, dev, dev_bf16, host, host_bits
+from gpu_helpers import attention_error, dev, dev_bf16, dev_meta, host, host_bits
 
 pytestmark = pytest.mark.gpu
 ATOL_MAX, ATOL_RMS = 2e-2, 2e-3
@@ -89,7 +89,7 @@ def gpu_bits(p, c, w, trig, given_scores):
         rs = np.ascontiguousarray(c["rows"].reshape(w.B, w.H, w.T * 64, w.T))
         ugbs.ugbs_select_rows(p, dev(trig), bm, row_scores=dev(rs))
     else:
-        ugbs.ugbs_select_rows(p, dev(trig), bm, Q=dev_bf16(c["inp"].Q), meta=dev_bf16(c["meta"]))
+        ugbs.ugbs_select_rows(p, dev(trig), bm, Q=dev_bf16(c["inp"].Q), meta=dev_meta(c["meta"]))
     torch.cuda.synchronize()
     return host(bm).view(np.uint32)
 
@@ -249,7 +249,7 @@ def test_full_size_row_selection(name):
     inp = synth.generate(w, threads=16)
     p = problem(w)
     Q, K, V = dev_bf16(inp.Q), dev_bf16(inp.K), dev_bf16(inp.V)
-    meta = torch.empty((w.B, w.Hkv, w.NB, p.meta_width, w.d), dtype=torch.bfloat16, device="cuda")
+    meta = torch.empty((w.B, w.Hkv, w.NB, w.d, p.meta_width), dtype=torch.bfloat16, device="cuda")
     ugbs.ugbs_block_meta(p, K, meta)
     trig = torch.zeros((w.B, w.T), dtype=torch.uint8, device="cuda")
     bm = torch.empty((w.B, w.H, w.T, ugbs.bitmap_words(p)), dtype=torch.int32, device="cuda")
