@@ -40,6 +40,11 @@ CFLAGS = [
     "-Wall", "-Wno-unused-function",
 ]
 
+# Per-source additions.  The scoring kernels keep their MFMA accumulators in
+# VGPRs, where the tile max reads them (no accumulator-register copies); the
+# attention kernel needs the accumulator registers for its budget.
+EXTRA_FLAGS = {"score_select.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
 PACKED_FP32 = re.compile(r"\bv_pk_(add|mul|fma)_f32\b")
 
 
@@ -87,7 +92,7 @@ def check_no_packed_fp32(obj: str) -> int:
 
 def _compile(src, verbose):
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [_hipcc(), *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [_hipcc(), *CFLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

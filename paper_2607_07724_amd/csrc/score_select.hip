@@ -250,27 +250,40 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
     const int nchunks = (nc_top + MC::kBlocks - 1) / MC::kBlocks;
     // this wave issues the chunk's 1 KiB loads i = w, w + GW, ...
     const int n_mine = (MC::kLoads - w + P.GW - 1) / P.GW;
-    // this wave's share of a chunk: loads i = w, w + GW, ...; the lane
-    // offsets within the chunk are recomputed per issue (a few integer
-    // operations), only the base moves
+    // this wave's share of a chunk: loads i = w, w + GW, ... (at most
+    // kMine); the lane offsets within a chunk are the same for every chunk
+    // but the last, computed once
     constexpr int kMaxMine = MC::kLoads;
+    constexpr int kMine = MC::kLoads >= 4 ? MC::kLoads / 4 : 1;   // loads per wave of four
+    auto lane_off = [&](int i, int c, bool last) {
+      const int p = i * 64 + lane;                  // 16-byte LDS chunk of the slot
+      const int r = p / MC::CPR;                    // block row within the chunk
+      const int col = (p % MC::CPR) ^ (r & MC::SWZ);
+      // rows past the last candidate re-read the chunk's first row, which
+      // is a candidate (1 + kBlocks c <= nc_top for every issued chunk)
+      const int rr = (last && 1 + MC::kBlocks * c + r > nc_top) ? 0 : r;
+      return (uint32_t)((rr * KD + col * 8) * 2);
+    };
+    uint32_t off0[kMine];
+    const bool fast = P.GW == 4 && (MC::kLoads % 4) == 0;   // loads i = w + 4 j, j < kLoads / 4
+#pragma unroll
+    for (int j = 0; j < kMine; ++j) off0[j] = lane_off(w + 4 * j, 0, false);
     auto issue = [&](int c) {
       const uint32_t slot = ring_lds + (uint32_t)((c % kRing) * MC::kBytes);
       const uint16_t* base = mhead + (size_t)__builtin_amdgcn_readfirstlane(1 + MC::kBlocks * c) * KD;
       const bool last = MC::kBlocks * (c + 1) >= nc_top;   // workgroup-uniform
+      if (fast && !last) {
+#pragma unroll
+        for (int j = 0; j < kMine; ++j) {
+          const int i = w + 4 * j;
+          dma16(base, off0[j], __builtin_amdgcn_readfirstlane(slot + i * 1024));
+        }
+        return;
+      }
 #pragma unroll
       for (int j = 0; j < kMaxMine; ++j) {
         const int i = w + j * P.GW;
-        if (i < MC::kLoads) {
-          const int p = i * 64 + lane;                  // 16-byte LDS chunk of the slot
-          const int r = p / MC::CPR;                    // block row within the chunk
-          const int col = (p % MC::CPR) ^ (r & MC::SWZ);
-          // rows past the last candidate re-read the chunk's first row, which
-          // is a candidate (1 + kBlocks c <= nc_top for every issued chunk)
-          const int rr = (last && 1 + MC::kBlocks * c + r > nc_top) ? 0 : r;
-          const uint32_t off = (uint32_t)((rr * KD + col * 8) * 2);
-          dma16(base, off, __builtin_amdgcn_readfirstlane(slot + i * 1024));
-        }
+        if (i < MC::kLoads) dma16(base, lane_off(i, c, last), __builtin_amdgcn_readfirstlane(slot + i * 1024));
       }
     };
     for (int c = 0; c < kRing - 1 && c < nchunks; ++c) issue(c);
