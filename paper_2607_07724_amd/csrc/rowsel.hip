@@ -7,27 +7,72 @@
 // rows, handed to the attention kernel as a bitmap of N_B bits.
 //
 // One workgroup (16 waves) per (b, h, t) unit, kv head by kv head, heaviest
-// tile first.  The 64 rows go in four quarters of 16:
-//   scores     wave w computes the 16 x 16 score blocks of chunks w, w + 16,
-//              ... on bf16 MFMA (the 16 query rows in registers as the A
-//              operand, the chunk's metadata rows straight from L2 as the B
-//              operand; Quest as the 2:4-sparse contraction of quest_index
-//              on v_smfmac) into an LDS array [16 rows x N_B];
-//   selection  wave w takes row w: keys, the top-3 pre-filter and the radix
-//              threshold of the selection kernel (the survivors staged in
-//              the row's own LDS space once its keys are in registers), and
-//              an atomic OR of each kept block into the LDS bitmap.
+// tile first.  Two forms:
+//
+// Two passes over the scores (R <= kTwoPassMaxR), for a group of 64 rows
+// (32 at d = 256) whose queries are staged in LDS:
+//   pass 1   wave w computes the 64 x 16 score blocks of chunks w, w + 16,
+//            ... (16 candidate blocks each) on bf16 MFMA (the queries from
+//            LDS as the A operand, the chunk's metadata rows straight from L2
+//            as the B operand; Quest as the 2:4-sparse contraction of
+//            quest_index on v_smfmac) and keeps, per row, the maximum over
+//            its own columns: 256 streams per row, each the candidates
+//            16 c + j of one (wave, column j).  R of the stream maxima are
+//            R distinct scores, so the R-th largest of them is a lower bound
+//            L on the row's R-th largest score.
+//   pass 2   the same contraction again (same instructions, same values);
+//            the scores >= L go to the row's list in LDS with their
+//            positions (1.1 R - 1.5 R of them on the synthetic workloads; a
+//            bound cut to 16 key bits let 4% of the lists at R = 126 overflow).
+//   pass 3   wave w takes rows 4 w .. 4 w + 3 (2 w, 2 w + 1 at d = 256)
+//            together: the exact R-th largest key of each list by a radix
+//            descent from the list's common key prefix, ties at it by a
+//            radix over positions (lowest first), and an LDS OR of each
+//            kept block into the bitmap.
+//   Nothing of size N_B per row is stored; the metadata is read twice.  A
+//   list longer than kCap (many equal scores) sends its row to the quarter
+//   form below.
+//
+// Quarters (R > kTwoPassMaxR, and rows whose lists overflowed): the 64 rows
+// in four passes of 16; the waves compute the 16 x 16 score blocks of
+// interleaved chunks into an LDS array [16 rows x N_B], then wave w selects
+// row w with the keys, top-3 pre-filter and radix threshold of the
+// selection kernel.
+//
 // The bitmap words of blocks 0..t are then stored (the rest zero).
 #include "select_common.h"
 
 namespace ugbs {
 namespace {
 
-constexpr int kRowWaves = 16;  // four per SIMD, one row each: the selection is latency-bound
-constexpr int kQuarter = 16;                 // query rows per pass
+constexpr int kRowWaves = 16;  // four per SIMD: the selection steps are latency-bound
+constexpr int kQuarter = 16;                 // query rows per pass of the quarter form
 constexpr int kRowSlots = UGBS_MAX_BLOCKS_ROWS / 64;
-constexpr int kSurvivors = 256;               // pre-filter survivors per row
+constexpr int kSurvivors = 256;               // pre-filter survivors per row (quarter form)
 constexpr int kMinPitch = 2 * kSurvivors;     // floats: a row's LDS region holds its survivors
+constexpr int kStreams = 16 * kRowWaves;      // two-pass form: column streams per row
+constexpr int kCap = 256;                     // two-pass form: list entries per row
+constexpr int kTwoPassMaxR = 128;             // largest R of the two-pass form
+
+static_assert(kTwoPassMaxR < kStreams, "more streams than kept candidates, so the R-th stream maximum exists");
+
+// Two-pass geometry: rows per group (the A operands of a group's four or
+// two 16-row MFMA tiles come from LDS, and so do their Quest indices),
+// staged query row pitch with a 16-byte skew against bank conflicts, and the
+// LDS the form needs.
+template <int D>
+struct RowGeo {
+  static constexpr int RG = D == 256 ? 32 : 64;
+  static constexpr int RT = RG / 16;  // 16-row tiles per group = rows per wave in pass 3
+  static constexpr int QP = D + 8;
+  static constexpr int KS = D / 32;
+  static constexpr size_t kQBytes = sizeof(uint16_t) * RG * QP;
+  static constexpr size_t kIdxBytes = sizeof(uint32_t) * RT * KS * 64;  // Quest indices per (tile, k-step, lane)
+  static constexpr size_t kBytes = kQBytes + kIdxBytes + sizeof(uint64_t) * RG * kCap;
+  static_assert(kQBytes % 16 == 0 && kIdxBytes % 16 == 0, "the lists start 16-byte aligned");
+  static_assert(RT * KS * 64 <= 64 * kRowWaves, "one index word per thread");
+  static_assert(sizeof(uint32_t) * kStreams <= sizeof(uint64_t) * kCap, "stream maxima fit the list space");
+};
 
 struct RowParams {
   Shape s;
@@ -37,8 +82,61 @@ struct RowParams {
   const uint8_t* trigger;   // [B, T] trigger flags
   uint32_t* bitmap;         // [B, H, T, nw]
   int nw;
-  int pitch;                // floats per LDS score row (>= kMinPitch)
+  int pitch;                // floats per LDS score row of the quarter form (>= kMinPitch)
 };
+
+// Wave-wide maximum / minimum of 32-bit keys (xor butterfly through the LDS
+// crossbar), uniform across the wave.
+__device__ __forceinline__ uint32_t wave_max_key(uint32_t x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x = max(x, (uint32_t)__shfl_xor((int)x, m));
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)x);
+}
+
+__device__ __forceinline__ uint32_t wave_min_key(uint32_t x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x = min(x, (uint32_t)__shfl_xor((int)x, m));
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)x);
+}
+
+// Common prefix of the keys in [lo, hi]: the bits above the highest bit in
+// which lo and hi differ, and that bit (-1 when lo == hi).
+__device__ __forceinline__ uint32_t key_prefix(uint32_t lo, uint32_t hi, int* top) {
+  if (lo == hi) {
+    *top = -1;
+    return hi;
+  }
+  const int sb = 31 - __builtin_clz(lo ^ hi);
+  *top = sb;
+  return sb == 31 ? 0u : hi & ~((2u << sb) - 1u);
+}
+
+// Radix descent of M rows at once (independent chains, interleaved): for
+// every row j, the largest thr[j] with at least R of key[j][..] >= thr[j],
+// resolved from bit top down to bit stop.  thr[j] enters holding the row's
+// common key prefix; a bit inside a row's prefix leaves its thr unchanged
+// (every key has it, or none), so all rows descend from the highest top.
+// Empty entries hold key 0 and never count (every candidate is >= 1).
+template <int M, int S>
+__device__ __forceinline__ void descend(const uint32_t (&key)[M][S], uint32_t (&thr)[M], int R, int top,
+                                        int stop) {
+  for (int bit = top; bit >= stop; --bit) {
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+      const uint32_t cand = thr[j] | (1u << bit);
+      int cnt = 0;
+#pragma unroll
+      for (int sl = 0; sl < S; ++sl) cnt += (int)__popcll(__ballot(key[j][sl] >= cand));
+      thr[j] = cnt >= R ? cand : thr[j];
+    }
+  }
+}
+
+// The score at or above which a score's key is >= the bound key L (keys of
+// finite scores are >= 0x00800000; a smaller L admits every score).
+__device__ __forceinline__ float bound_value(uint32_t L) {
+  return L < 0x00800000u ? -__builtin_inff() : key_value(L);
+}
 
 // The R best keys of one row (positions 0..nc-1 = blocks 1..nc) set in bits.
 __device__ __forceinline__ void row_top(const float* row, int nc, int R, int lane_in, uint32_t* bits,
@@ -107,18 +205,326 @@ __device__ __forceinline__ void row_top(const float* row, int nc, int R, int lan
     });
 }
 
-template <int D, bool QUEST>
+// Quarter form for the rows set in rowmask (bit r = row r of the tile).
+template <int D, bool QUEST, bool GIVEN>
+__device__ void quarter_rows(const RowParams& P, float* s_rows, uint32_t* s_bits, const uint16_t* mhead,
+                             const uint16_t* qtile, size_t rowbase, int nc, int R, uint64_t rowmask, int w,
+                             int lane) {
+  constexpr int KD = QUEST ? 2 * D : D;  // metadata row length
+  constexpr int KS = D / 32;             // k-steps of 32 channels (raw query rows)
+  const int g = lane >> 4, c16 = lane & 15;
+  const int nchunks = (nc + 15) / 16;
+  for (int qr = 0; qr < kBlock / kQuarter; ++qr) {
+    const uint32_t qmask = (uint32_t)(rowmask >> (kQuarter * qr)) & 0xffffu;
+    if (qmask == 0u) continue;
+    const float* rows;  // 16 rows of scores of this quarter, row stride `stride`
+    size_t stride;
+    if constexpr (GIVEN) {
+      rows = P.row_scores + (rowbase + (size_t)kQuarter * qr) * P.s.NB + 1;
+      stride = P.s.NB;
+    } else {
+      // ---- scores of rows 16 qr .. 16 qr + 15, chunk by chunk --------------
+      bf16x8 a[KS];
+      uint32_t qidx[QUEST ? KS : 1];
+      const uint16_t* qrow = qtile + (size_t)(kQuarter * qr + c16) * D;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g);
+        a[ks] = as_bf16x8(v);
+        if constexpr (QUEST) qidx[ks] = quest_index(v);
+      }
+      // the chunk's metadata rows straight from L2 as the B operand; Quest:
+      // per k-step the (kmin, kmax) pairs of channels 32 ks + 4 g .. + 3 and
+      // 32 ks + 16 + 4 g .. + 3 (see quest_index)
+      constexpr int KB = QUEST ? 2 * KS : KS;
+      for (int c = w; c < nchunks; c += kRowWaves) {
+        const int p = 16 * c + c16;  // block 1 + p; past the last candidate block 1 is read
+        const uint16_t* mrow = mhead + (size_t)(1 + (p < nc ? p : 0)) * KD;
+        uint4 cur[KB];
+#pragma unroll
+        for (int j = 0; j < KB; ++j)
+          cur[j] = *reinterpret_cast<const uint4*>(mrow + (QUEST ? 64 * (j / 2) + 32 * (j % 2) + 8 * g
+                                                                 : 32 * j + 8 * g));
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+        if constexpr (QUEST) {
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[ks], as_bf16x16(cur[2 * ks], cur[2 * ks + 1]), acc,
+                                                            (int)qidx[ks], 0, 0);
+        } else {
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks], as_bf16x8(cur[ks]), acc, 0, 0, 0);
+        }
+        // lane holds rows 4g + i of the quarter, block column c16
+        if (p < nc) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) s_rows[(4 * g + i) * P.pitch + p] = acc[i];
+        }
+      }
+      __syncthreads();
+      rows = s_rows;
+      stride = (size_t)P.pitch;
+    }
+    // ---- selection: wave w takes row w --------------------------------------
+    for (int r = w; r < kQuarter; r += kRowWaves)
+      if ((qmask >> r) & 1u)
+        row_top(rows + (size_t)r * stride, nc, R, lane, s_bits,
+                reinterpret_cast<uint64_t*>(s_rows + (size_t)r * P.pitch));
+    __syncthreads();  // s_rows is rewritten by the next quarter
+  }
+}
+
+// Two-pass form for all 64 rows of the tile; the rows whose lists overflowed
+// are left set in the 64-bit mask s_small[128..129] for the quarter form.
+template <int D, bool QUEST, bool GIVEN>
+__device__ void two_pass_rows(const RowParams& P, unsigned char* s_dyn, uint32_t* s_bits, uint32_t* s_small,
+                              const uint16_t* mhead, const uint16_t* qtile, size_t rowbase, int nc, int R,
+                              int w, int lane) {
+  using G = RowGeo<D>;
+  constexpr int KD = QUEST ? 2 * D : D;
+  constexpr int KS = G::KS, RT = G::RT, RG = G::RG;
+  constexpr int KB = QUEST ? 2 * KS : KS;
+  uint16_t* s_q = reinterpret_cast<uint16_t*>(s_dyn);                     // [RG][QP] staged queries
+  uint32_t* s_qidx = reinterpret_cast<uint32_t*>(s_dyn + G::kQBytes);     // [RT][KS][64]  Quest indices
+  unsigned char* s_r = s_dyn + G::kQBytes + G::kIdxBytes;
+  uint32_t* s_max = reinterpret_cast<uint32_t*>(s_r);                     // [RG][kStreams] pass 1
+  uint64_t* s_list = reinterpret_cast<uint64_t*>(s_r);                    // [RG][kCap]     pass 2, 3
+  uint32_t* s_cnt = s_small;            // [64] list lengths
+  uint32_t* s_bound = s_small + 64;     // [64] bound keys L
+  uint32_t* s_over = s_small + 128;     // [2]  overflowed rows (bit mask)
+  float* s_fbound = reinterpret_cast<float*>(s_small + 132);  // [64] bounds as scores (16-byte aligned)
+  const int g = lane >> 4, c16 = lane & 15;
+  const int nchunks = (nc + 15) / 16;
+  const int NB = P.s.NB;
+
+  for (int row0 = 0; row0 < kBlock; row0 += RG) {
+    if constexpr (!GIVEN) {
+      const uint16_t* src = qtile + (size_t)row0 * D;
+      for (int i = threadIdx.x; i < RG * D / 8; i += 64 * kRowWaves) {
+        const int r = i / (D / 8), c = i % (D / 8);
+        *reinterpret_cast<uint4*>(s_q + r * G::QP + 8 * c) = *reinterpret_cast<const uint4*>(src + (size_t)r * D + 8 * c);
+      }
+    }
+    if (threadIdx.x < RG) s_cnt[threadIdx.x] = 0u;
+    __syncthreads();
+
+    // A operand of tile rt, k-step ks: row 16 rt + c16, channels 32 ks + 8 g ..
+    // (z: an opaque zero per chunk, so the loads are not hoisted out of the
+    // chunk loop into registers the loop cannot spare)
+    auto a_op = [&](int rt, int ks, int z) {
+      return *reinterpret_cast<const uint4*>(s_q + (16 * rt + c16) * G::QP + 32 * ks + 8 * g + z);
+    };
+    if constexpr (QUEST && !GIVEN) {
+      {
+        if (threadIdx.x < RT * KS * 64) {
+          const int ln = threadIdx.x & 63, rk = threadIdx.x >> 6;  // rk = KS rt + ks
+          const int rt = rk / KS, ks = rk % KS;
+          s_qidx[threadIdx.x] = quest_index(*reinterpret_cast<const uint4*>(
+              s_q + (16 * rt + (ln & 15)) * G::QP + 32 * ks + 8 * (ln >> 4)));
+        }
+        __syncthreads();
+      }
+    }
+    // scores of chunk c: lane holds rows 16 rt + 4 g + i of the group, column
+    // c16 (candidate p = 16 c + c16, block 1 + p); entries with p >= nc are
+    // unused (block 1 is read in their place)
+    auto chunk = [&](int c, f32x4 (&acc)[RT]) {
+      const int p = 16 * c + c16;
+      if constexpr (GIVEN) {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            acc[rt][i] = p < nc ? P.row_scores[(rowbase + row0 + 16 * rt + 4 * g + i) * NB + 1 + p] : 0.f;
+      } else {
+        int z = 0;
+        asm volatile("" : "+v"(z));
+        const uint16_t* mrow = mhead + (size_t)(1 + (p < nc ? p : 0)) * KD;
+        uint4 b[KB];
+#pragma unroll
+        for (int j = 0; j < KB; ++j)
+          b[j] = *reinterpret_cast<const uint4*>(mrow + (QUEST ? 64 * (j / 2) + 32 * (j % 2) + 8 * g : 32 * j + 8 * g));
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt) {
+            if constexpr (QUEST)
+              acc[rt] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(as_bf16x8(a_op(rt, ks, z)),
+                                                                  as_bf16x16(b[2 * ks], b[2 * ks + 1]), acc[rt],
+                                                                  (int)s_qidx[(KS * rt + ks) * 64 + lane + z], 0, 0);
+            else
+              acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a_op(rt, ks, z)), as_bf16x8(b[ks]), acc[rt],
+                                                                0, 0, 0);
+          }
+        }
+      }
+    };
+
+    // ---- pass 1: stream maxima ----------------------------------------------
+    {
+      float mx[RT][4];
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mx[rt][i] = -__builtin_inff();
+      for (int c = w; c < nchunks; c += kRowWaves) {
+        f32x4 acc[RT];
+        chunk(c, acc);
+        const bool in = 16 * c + c16 < nc;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) mx[rt][i] = fmaxf(mx[rt][i], in ? acc[rt][i] : -__builtin_inff());
+      }
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          s_max[(16 * rt + 4 * g + i) * kStreams + 16 * w + c16] =
+              mx[rt][i] == -__builtin_inff() ? 0u : order_key(mx[rt][i]);
+    }
+    __syncthreads();
+
+    // ---- bounds: wave w, rows RT w + j ---------------------------------------
+    {
+      uint32_t key[RT][kStreams / 64], thr[RT];
+      int top = -1;
+#pragma unroll
+      for (int j = 0; j < RT; ++j) {
+        uint32_t hi = 0u, lo = 0xffffffffu;
+#pragma unroll
+        for (int sl = 0; sl < kStreams / 64; ++sl) {
+          key[j][sl] = s_max[(RT * w + j) * kStreams + 64 * sl + lane];
+          hi = max(hi, key[j][sl]);
+          lo = min(lo, key[j][sl] == 0u ? 0xffffffffu : key[j][sl]);
+        }
+        int tj;
+        thr[j] = key_prefix(wave_min_key(lo), wave_max_key(hi), &tj);
+        top = tj > top ? tj : top;
+      }
+      descend<RT, kStreams / 64>(key, thr, R, top, 0);
+      if (lane == 0) {
+#pragma unroll
+        for (int j = 0; j < RT; ++j) s_bound[RT * w + j] = thr[j];
+      }
+    }
+    __syncthreads();  // the stream maxima are read: the lists take their space
+
+    // ---- pass 2: lists of the scores >= L ------------------------------------
+    {
+      if (threadIdx.x < RG) s_fbound[threadIdx.x] = bound_value(s_bound[threadIdx.x]);
+      __syncthreads();
+      for (int c = w; c < nchunks; c += kRowWaves) {
+        f32x4 acc[RT];
+        chunk(c, acc);
+        const int p = 16 * c + c16;
+        if (p < nc) {
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt) {
+            // the bounds of rows 16 rt + 4 g .. + 3, re-read per chunk (not
+            // held across the loop: registers)
+            const float4 fb = *reinterpret_cast<const float4*>(s_fbound + 16 * rt + 4 * g);
+            const float fl[4] = {fb.x, fb.y, fb.z, fb.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              if (acc[rt][i] >= fl[i]) {
+                const int r = 16 * rt + 4 * g + i;
+                const uint32_t at = atomicAdd(&s_cnt[r], 1u);
+                if (at < (uint32_t)kCap) s_list[r * kCap + at] = ((uint64_t)order_key(acc[rt][i]) << 32) | (uint32_t)p;
+              }
+            }
+          }
+        }
+      }
+    }
+    __syncthreads();
+
+    // ---- pass 3: exact top R of each list ------------------------------------
+    {
+      constexpr int SL = kCap / 64;
+      uint32_t key[RT][SL], pos[RT][SL], thr[RT];
+      int n[RT];
+      int top = -1;
+#pragma unroll
+      for (int j = 0; j < RT; ++j) {
+        const int r = RT * w + j;
+        n[j] = __builtin_amdgcn_readfirstlane((int)s_cnt[r]);
+        // a list shorter than R cannot happen (pass 2 recomputes pass 1's
+        // scores exactly); it is sent to the quarter form like an overflow
+        const bool ok = n[j] >= R && n[j] <= kCap;
+        uint32_t hi = 0u, lo = 0xffffffffu;
+#pragma unroll
+        for (int sl = 0; sl < SL; ++sl) {
+          const int e = 64 * sl + lane;
+          const uint64_t v = (ok && e < n[j]) ? s_list[r * kCap + e] : 0ull;
+          key[j][sl] = (uint32_t)(v >> 32);
+          pos[j][sl] = (uint32_t)v;
+          hi = max(hi, key[j][sl]);
+          lo = min(lo, key[j][sl] == 0u ? 0xffffffffu : key[j][sl]);
+        }
+        int tj = -1;
+        thr[j] = 0u;
+        if (ok) {
+          thr[j] = key_prefix(wave_min_key(lo), wave_max_key(hi), &tj);
+        } else if (lane == 0) {
+          atomicOr(&s_over[(row0 + r) >> 5], 1u << ((row0 + r) & 31));
+        }
+        n[j] = ok ? n[j] : 0;
+        top = tj > top ? tj : top;
+      }
+      descend<RT, SL>(key, thr, R, top, 0);
+#pragma unroll
+      for (int j = 0; j < RT; ++j) {
+        if (n[j] == 0) continue;
+        int above = 0, eq = 0;
+#pragma unroll
+        for (int sl = 0; sl < SL; ++sl) {
+          above += (int)__popcll(__ballot(key[j][sl] > thr[j]));
+          eq += (int)__popcll(__ballot(key[j][sl] == thr[j]));
+        }
+        // the keys equal to thr are taken lowest position first: the need-th
+        // smallest of their positions (positions < 2048) by a radix descent
+        uint32_t last = 0xffffffffu;
+        if (above + eq > R) {
+          const int need = R - above;
+          uint32_t lo = 0u;
+          for (int bit = 10; bit >= 0; --bit) {
+            int c = 0;
+#pragma unroll
+            for (int sl = 0; sl < SL; ++sl)
+              c += (int)__popcll(__ballot(key[j][sl] == thr[j] && pos[j][sl] < lo + (1u << bit)));
+            if (c < need) lo += 1u << bit;
+          }
+          last = lo;
+        }
+#pragma unroll
+        for (int sl = 0; sl < SL; ++sl) {
+          if (key[j][sl] > thr[j] || (key[j][sl] == thr[j] && pos[j][sl] <= last)) {
+            const int blk = 1 + (int)pos[j][sl];
+            atomicOr(&s_bits[blk >> 5], 1u << (blk & 31));
+          }
+        }
+      }
+    }
+    __syncthreads();  // the lists and queries are rewritten by the next group
+  }
+}
+
+// GIVEN: the scores come from P.row_scores (D and QUEST then unused)
+template <int D, bool QUEST, bool GIVEN>
 __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
-  constexpr int KD = QUEST ? 2 * D : D;        // metadata row length
-  constexpr int KS = D / 32;                   // k-steps of 32 channels (raw query rows)
-  // [16][pitch]: the quarter's scores; row r's region then holds the
-  // survivors of row r (also when the scores come from memory)
-  extern __shared__ __align__(16) float s_rows[];
+  constexpr int KD = QUEST ? 2 * D : D;  // metadata row length
+  // quarter form: [16][pitch] scores of a quarter, row r's region then
+  // holding the survivors of row r; two-pass form: staged queries and lists
+  extern __shared__ __align__(16) unsigned char s_dyn[];
   __shared__ uint32_t s_bits[UGBS_MAX_BLOCKS_ROWS / 32];
+  __shared__ __align__(16) uint32_t s_small[196];
   const Shape& s = P.s;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int g = lane >> 4, c16 = lane & 15;
   const int n_units = s.B * s.H * s.T;
   const int uid = blockIdx.x;
   if (uid >= n_units) return;
@@ -133,6 +539,7 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
   const int nwords = (t >> 5) + 1;
 
   for (int i = threadIdx.x; i < P.nw; i += 64 * kRowWaves) s_bits[i] = 0u;
+  if (threadIdx.x < 2) s_small[128 + threadIdx.x] = 0u;
   __syncthreads();
   if (threadIdx.x == 0) {
     atomicOr(&s_bits[0], 1u);
@@ -144,85 +551,33 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
     const int kvh = u.h / s.G;
     const uint16_t* mhead = P.meta + ((size_t)u.b * s.Hkv + kvh) * s.NB * KD;
     const uint16_t* qtile = P.Q + (((size_t)u.b * s.H + u.h) * s.N + (size_t)t * kBlock) * D;
-    const int nchunks = (nc + 15) / 16;
-    for (int qr = 0; qr < kBlock / kQuarter; ++qr) {
-      const float* rows;     // 16 rows of scores of this quarter, row stride `stride`
-      size_t stride;
-      if (P.row_scores) {
-        rows = P.row_scores + (((size_t)u.b * s.H + u.h) * s.N + (size_t)t * kBlock + kQuarter * qr) * s.NB + 1;
-        stride = s.NB;
-      } else {
-        // ---- scores of rows 16 qr .. 16 qr + 15, chunk by chunk ----------
-        bf16x8 a[KS];
-        uint32_t qidx[QUEST ? KS : 1];
-        const uint16_t* qrow = qtile + (size_t)(kQuarter * qr + c16) * D;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g);
-          a[ks] = as_bf16x8(v);
-          if constexpr (QUEST) qidx[ks] = quest_index(v);
-        }
-        // the chunk's metadata rows straight from L2 as the B operand; Quest:
-        // per k-step the (kmin, kmax) pairs of channels 32 ks + 4 g .. + 3 and
-        // 32 ks + 16 + 4 g .. + 3 (see quest_index)
-        constexpr int KB = QUEST ? 2 * KS : KS;
-        auto load_b = [&](int c, uint4 (&bv)[KB]) {
-          const int p = 16 * c + c16;  // block 1 + p; past the last candidate block 1 is read
-          const uint16_t* mrow = mhead + (size_t)(1 + (p < nc ? p : 0)) * KD;
-#pragma unroll
-          for (int j = 0; j < KB; ++j) {
-            const int off = QUEST ? 64 * (j / 2) + 32 * (j % 2) + 8 * g : 32 * j + 8 * g;
-            bv[j] = *reinterpret_cast<const uint4*>(mrow + off);
-          }
-        };
-        for (int c = w; c < nchunks; c += kRowWaves) {
-          uint4 cur[KB];
-          load_b(c, cur);
-          const int p = 16 * c + c16;
-          f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-          if constexpr (QUEST) {
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-              acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[ks], as_bf16x16(cur[2 * ks], cur[2 * ks + 1]), acc,
-                                                              (int)qidx[ks], 0, 0);
-          } else {
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-              acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks], as_bf16x8(cur[ks]), acc, 0, 0, 0);
-          }
-          // lane holds rows 4g + i of the quarter, block column c16
-          if (p < nc) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) s_rows[(4 * g + i) * P.pitch + p] = acc[i];
-          }
-        }
-        __syncthreads();
-        rows = s_rows;
-        stride = (size_t)P.pitch;
-      }
-      // ---- selection: wave w takes row w ------------------------------------
-      for (int r = w; r < kQuarter; r += kRowWaves)
-        row_top(rows + (size_t)r * stride, nc, R, lane, s_bits,
-                reinterpret_cast<uint64_t*>(s_rows + (size_t)r * P.pitch));
-      __syncthreads();  // s_rows is rewritten by the next quarter
+    const size_t rowbase = ((size_t)u.b * s.H + u.h) * s.N + (size_t)t * kBlock;
+    uint64_t rest = ~0ull;  // rows for the quarter form
+    if (R <= kTwoPassMaxR) {
+      two_pass_rows<D, QUEST, GIVEN>(P, s_dyn, s_bits, s_small, mhead, qtile, rowbase, nc, R, w, lane);
+      rest = ((uint64_t)s_small[129] << 32) | s_small[128];  // read after the last barrier of the pass
     }
+    if (rest != 0ull)
+      quarter_rows<D, QUEST, GIVEN>(P, reinterpret_cast<float*>(s_dyn), s_bits, mhead, qtile, rowbase, nc, R, rest, w,
+                             lane);
   }
   __syncthreads();
   uint32_t* out = P.bitmap + rowid * P.nw;
   for (int i = threadIdx.x; i < P.nw; i += 64 * kRowWaves) out[i] = (i < nwords) ? s_bits[i] : 0u;
 }
 
-template <int D, bool QUEST>
+template <int D, bool QUEST, bool GIVEN>
 hipError_t launch_rows(RowParams P, hipStream_t stream) {
-  const size_t smem = sizeof(float) * (size_t)kQuarter * P.pitch;
-  if (smem + sizeof(uint32_t) * (UGBS_MAX_BLOCKS_ROWS / 32) > 65536) {
-    const hipError_t e = hipFuncSetAttribute((const void*)rowsel_kernel<D, QUEST>,
+  const size_t smem = std::max(sizeof(float) * (size_t)kQuarter * P.pitch, RowGeo<D>::kBytes);
+  const size_t fixed = sizeof(uint32_t) * (UGBS_MAX_BLOCKS_ROWS / 32 + 196);
+  if (smem + fixed > 65536) {
+    const hipError_t e = hipFuncSetAttribute((const void*)rowsel_kernel<D, QUEST, GIVEN>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
   }
   const int n_units = P.s.B * P.s.H * P.s.T;
   const int grid = ((n_units + 7) / 8) * 8;
-  rowsel_kernel<D, QUEST><<<grid, 64 * kRowWaves, smem, stream>>>(P);
+  rowsel_kernel<D, QUEST, GIVEN><<<grid, 64 * kRowWaves, smem, stream>>>(P);
   return hipGetLastError();
 }
 
@@ -242,10 +597,11 @@ hipError_t launch_select_rows(const Shape& s, const uint16_t* Q, const uint16_t*
   // padded against bank conflicts of the column writes; with scores from
   // memory the rows only hold survivors
   P.pitch = row_scores ? kMinPitch : std::max(((s.NB + 3) & ~3) + 4, kMinPitch);
+  if (row_scores) return launch_rows<64, false, true>(P, stream);
   const bool quest = s.backbone == UGBS_QUEST;
-  if (s.d == 256) return quest ? launch_rows<256, true>(P, stream) : launch_rows<256, false>(P, stream);
-  if (s.d == 128) return quest ? launch_rows<128, true>(P, stream) : launch_rows<128, false>(P, stream);
-  return quest ? launch_rows<64, true>(P, stream) : launch_rows<64, false>(P, stream);
+  if (s.d == 256) return quest ? launch_rows<256, true, false>(P, stream) : launch_rows<256, false, false>(P, stream);
+  if (s.d == 128) return quest ? launch_rows<128, true, false>(P, stream) : launch_rows<128, false, false>(P, stream);
+  return quest ? launch_rows<64, true, false>(P, stream) : launch_rows<64, false, false>(P, stream);
 }
 
 }  // namespace ugbs

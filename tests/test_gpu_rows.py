@@ -236,6 +236,100 @@ def test_layer_with_row_selection(name):
     assert same >= 0.9 * w.B * w.H * w.T
 
 
+def _row_mix(g, n_rows, NB):
+    """Row scores of five shapes, drawn per row: Gaussian; a coarse grid
+    (many equal scores); zeros of both signs; a constant with 5% outliers;
+    large negative values with a small spread."""
+    x = g.standard_normal((n_rows, NB)).astype(np.float32)
+    kind = g.integers(0, 5, n_rows)
+    m = kind == 1
+    x[m] = np.round(x[m] * 2) / 2
+    m = kind == 2
+    x[m] = np.where(g.random((int(m.sum()), NB)) < 0.5, np.float32(0.0), np.float32(-0.0))
+    m = kind == 3
+    x[m] = np.float32(1.5) + (g.random((int(m.sum()), NB)) < 0.05) * x[m]
+    m = kind == 4
+    x[m] = x[m] * np.float32(1e30) - np.float32(1e35)
+    return x
+
+
+LONG_TILES = [0, 1, 2, 3, 4, 63, 64, 65, 66, 127, 128, 129, 130, 131, 200, 255, 256, 257, 258, 259,
+              300, 400, 450, 511]
+
+
+@pytest.mark.parametrize("k,rho,mode", [(3, 2, "none"), (64, 2, "none"), (64, 2, "all"), (64, 3, "all"),
+                                        (100, 2, "route")])
+def test_given_scores_long_rows_bit_exact(k, rho, mode):
+    """512 tiles: R from 1 to 190, so the two-pass form (R <= 128), its
+    lists overflowing (grid, zero and constant rows beyond 256 candidates:
+    those rows go to the quarter form) and the quarter form for R > 128 (k
+    100 with routed flags mixes both in one launch); bitmaps of sampled
+    tiles bit-exact against the oracle on the same scores."""
+    torch = __import__("torch")
+    B, H, T = 1, 2, 512
+    N = 64 * T
+    g = np.random.default_rng(700 + 10 * k + rho)
+    rs = _row_mix(g, B * H * N, T).reshape(B, H, N, T)
+    if mode == "route":
+        trig = (g.random((B, T)) < 0.5).astype(np.uint8)
+    else:
+        trig = np.full((B, T), 1 if mode == "all" else 0, np.uint8)
+    p = ugbs.Problem.make(B, H, H, N, 64, k, 0.1, synth.KMEAN, rho=rho)
+    bm = torch.full((B, H, T, ugbs.bitmap_words(p)), -1, dtype=torch.int32, device="cuda")
+    ugbs.ugbs_select_rows(p, dev(trig), bm, row_scores=dev(rs))
+    torch.cuda.synchronize()
+    gb = host(bm).view(np.uint32)
+    units = [(0, h, t) for h in range(H) for t in LONG_TILES]
+    rows = np.stack([rs[b, h, 64 * t:64 * t + 64] for b, h, t in units])
+    ob = oracle.select_rows(rows, [t for _, _, t in units], k, rho, [trig[b, t] for b, _, t in units])
+    for i, (b, h, t) in enumerate(units):
+        assert np.array_equal(gb[b, h, t], ob[i]), (h, t)
+    # the words after tile t's are zero
+    for b, h, t in units:
+        assert not gb[b, h, t, t // 32 + 1:].any()
+
+
+MEDIUM = {
+    "quest_d128": synth.Workload("R5", 1, 4, 2, 128, 32768, 64, 0.25, synth.QUEST, "mixture",
+                                 needles=4, base_seed=65),
+    "kmean_d256": synth.Workload("R6", 1, 2, 1, 256, 32768, 64, 0.25, synth.KMEAN, "offset",
+                                 needles=4, base_seed=66),
+    "quest_d64": synth.Workload("R7", 1, 4, 1, 64, 32768, 64, 0.25, synth.QUEST, "offset",
+                                needles=4, base_seed=67),
+}
+
+
+@pytest.mark.parametrize("name", list(MEDIUM))
+@pytest.mark.parametrize("mode", ["none", "all"])
+def test_computed_scores_long_rows(name, mode):
+    """512 tiles with the scores computed on the GPU (both row groups of the
+    d = 256 form), R = 62 / 126: sampled tiles against the oracle up to
+    near-ties."""
+    torch = __import__("torch")
+    w = MEDIUM[name]
+    inp = synth.generate(w, threads=8)
+    p = problem(w)
+    Q, K = dev_bf16(inp.Q), dev_bf16(inp.K)
+    meta = torch.empty((w.B, w.Hkv, w.NB, w.d, p.meta_width), dtype=torch.bfloat16, device="cuda")
+    ugbs.ugbs_block_meta(p, K, meta)
+    trig = np.full((w.B, w.T), 1 if mode == "all" else 0, np.uint8)
+    bm = torch.full((w.B, w.H, w.T, ugbs.bitmap_words(p)), -1, dtype=torch.int32, device="cuda")
+    ugbs.ugbs_select_rows(p, dev(trig), bm, Q=Q, meta=meta)
+    torch.cuda.synchronize()
+    gb = host(bm).view(np.uint32)
+    units = np.array([(0, h, t) for h in range(w.H) for t in LONG_TILES[::2]], np.int32)
+    meta_np = oracle.block_meta(w.backbone, inp.K, nthreads=8)
+    rows = oracle.row_scores(w.backbone, inp.Q, meta_np, w.Hkv, units=units, nthreads=8)
+    ob = oracle.select_rows(rows, units[:, 2], w.k, w.rho, trig[0, units[:, 2]])
+    k_eff = w.rho * w.k if mode == "all" else w.k
+    exempt = 0
+    for i, (b, h, t) in enumerate(units):
+        ok, nd = near_tie_bits_ok(gb[b, h, t], ob[i], rows[i], int(t), k_eff)
+        assert ok, (b, h, t)
+        exempt += nd > 0
+    assert exempt <= 2
+
+
 @pytest.mark.slow
 @pytest.mark.parametrize("name", ["C2", "C4"])
 def test_full_size_row_selection(name):
