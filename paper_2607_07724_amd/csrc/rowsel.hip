@@ -9,26 +9,25 @@
 // One workgroup (16 waves) per (b, h, t) unit, kv head by kv head, heaviest
 // tile first.  Two forms:
 //
-// Two passes over the scores (R <= kTwoPassMaxR), for a group of 64 rows
-// (32 at d = 256) whose queries are staged in LDS:
-//   pass 1   wave w computes the 64 x 16 score blocks of chunks w, w + 16,
-//            ... (16 candidate blocks each) on bf16 MFMA (the queries from
-//            LDS as the A operand, the chunk's metadata rows straight from L2
-//            as the B operand; Quest as the 2:4-sparse contraction of
-//            quest_index on v_smfmac) and keeps, per row, the maximum over
-//            its own columns: 256 streams per row, each the candidates
-//            16 c + j of one (wave, column j).  R of the stream maxima are
-//            R distinct scores, so the R-th largest of them is a lower bound
-//            L on the row's R-th largest score.
+// Two passes over the scores (R <= kTwoPassMaxR).  The candidates stream
+// through an LDS ring in super-chunks of 64 consecutive blocks (1 KiB
+// direct-to-LDS loads shared by the workgroup); wave w computes row tile
+// w mod 4 (its 16 query rows in registers as the A operand) against column
+// tile w / 4 of every super-chunk on bf16 MFMA (Quest as the 2:4-sparse
+// contraction of quest_index on v_smfmac), so a lane sees, for 4 rows, the
+// candidates p = 64 m + j of one stream j (64 streams per row).
+//   pass 1   every lane keeps the 4 largest scores of each of its (row,
+//            stream) pairs.  Any R of these 256 values per row are R
+//            distinct scores of the row, so their R-th largest is a lower
+//            bound L on the row's R-th largest score.
 //   pass 2   the same contraction again (same instructions, same values);
 //            the scores >= L go to the row's list in LDS with their
-//            positions (1.1 R - 1.5 R of them on the synthetic workloads; a
-//            bound cut to 16 key bits let 4% of the lists at R = 126 overflow).
-//   pass 3   wave w takes rows 4 w .. 4 w + 3 (2 w, 2 w + 1 at d = 256)
-//            together: the exact R-th largest key of each list by a radix
+//            positions (1.00 R - 1.02 R of them on the synthetic workloads).
+//   pass 3   wave w takes rows 4 w .. 4 w + 3 together: a list of exactly R
+//            is kept whole; otherwise the exact R-th largest key by a radix
 //            descent from the list's common key prefix, ties at it by a
-//            radix over positions (lowest first), and an LDS OR of each
-//            kept block into the bitmap.
+//            radix over positions (lowest first).  Kept blocks are ORed
+//            into the LDS bitmap.
 //   Nothing of size N_B per row is stored; the metadata is read twice.  A
 //   list longer than kCap (many equal scores) sends its row to the quarter
 //   form below.
@@ -40,7 +39,7 @@
 // selection kernel.
 //
 // The bitmap words of blocks 0..t are then stored (the rest zero).
-#include "select_common.h"
+#include "attend_common.h"
 
 namespace ugbs {
 namespace {
@@ -50,29 +49,35 @@ constexpr int kQuarter = 16;                 // query rows per pass of the quart
 constexpr int kRowSlots = UGBS_MAX_BLOCKS_ROWS / 64;
 constexpr int kSurvivors = 256;               // pre-filter survivors per row (quarter form)
 constexpr int kMinPitch = 2 * kSurvivors;     // floats: a row's LDS region holds its survivors
-constexpr int kStreams = 16 * kRowWaves;      // two-pass form: column streams per row
-constexpr int kCap = 256;                     // two-pass form: list entries per row
+constexpr int kStreams = 64;                  // two-pass form: column streams per row
+constexpr int kTop = 4;                       // largest scores kept per (row, stream)
+constexpr int kBoundVals = kStreams * kTop;   // values per row the lower bound is taken over
+constexpr int kCap = 176;                     // two-pass form: list entries per row
 constexpr int kTwoPassMaxR = 128;             // largest R of the two-pass form
+constexpr int kRegionA = 65536;               // metadata ring, then the per-row stream values
 
-static_assert(kTwoPassMaxR < kStreams, "more streams than kept candidates, so the R-th stream maximum exists");
+static_assert(kTwoPassMaxR < kBoundVals, "more bound values than kept candidates");
+static_assert(sizeof(uint32_t) * kBlock * kBoundVals <= kRegionA, "stream values fit the ring's space");
+static_assert(kRowWaves == 16 && kStreams == 64, "16 waves: four row tiles x four 16-column tiles");
 
-// Two-pass geometry: rows per group (the A operands of a group's four or
-// two 16-row MFMA tiles come from LDS, and so do their Quest indices),
-// staged query row pitch with a 16-byte skew against bank conflicts, and the
-// LDS the form needs.
-template <int D>
-struct RowGeo {
-  static constexpr int RG = D == 256 ? 32 : 64;
-  static constexpr int RT = RG / 16;  // 16-row tiles per group = rows per wave in pass 3
-  static constexpr int QP = D + 8;
-  static constexpr int KS = D / 32;
-  static constexpr size_t kQBytes = sizeof(uint16_t) * RG * QP;
-  static constexpr size_t kIdxBytes = sizeof(uint32_t) * RT * KS * 64;  // Quest indices per (tile, k-step, lane)
-  static constexpr size_t kBytes = kQBytes + kIdxBytes + sizeof(uint64_t) * RG * kCap;
-  static_assert(kQBytes % 16 == 0 && kIdxBytes % 16 == 0, "the lists start 16-byte aligned");
-  static_assert(RT * KS * 64 <= 64 * kRowWaves, "one index word per thread");
-  static_assert(sizeof(uint32_t) * kStreams <= sizeof(uint64_t) * kCap, "stream maxima fit the list space");
+// Two-pass metadata super-chunk: 64 consecutive candidate blocks, fetched
+// into LDS by the workgroup with 1 KiB direct loads, rows as 16-byte columns
+// XOR-swizzled by row (conflict-free B reads); two ring slots where they fit
+// in kRegionA (one at d = 256 Quest, 64 KiB per super-chunk).
+template <int D, bool QUEST>
+struct RowChunk {
+  static constexpr int kBlocks = 64;
+  static constexpr int KD = QUEST ? 2 * D : D;
+  static constexpr int CPR = KD / 8;
+  static constexpr int SWZ = (CPR < 16 ? CPR : 16) - 1;
+  static constexpr int kBytes = kBlocks * KD * 2;
+  static constexpr int kLoads = kBytes / 1024;
+  static constexpr int kRing = 2 * kBytes <= kRegionA ? 2 : 1;
+  static constexpr int kPerWave = (kLoads + kRowWaves - 1) / kRowWaves;
+  static_assert(kRing * kBytes <= kRegionA, "ring fits its region");
+  __device__ static __forceinline__ int off(int r, int c) { return (r * CPR + (c ^ (r & SWZ))) * 16; }
 };
+constexpr size_t kTwoPassBytes = kRegionA + sizeof(uint64_t) * kBlock * kCap;
 
 struct RowParams {
   Shape s;
@@ -112,22 +117,30 @@ __device__ __forceinline__ uint32_t key_prefix(uint32_t lo, uint32_t hi, int* to
 }
 
 // Radix descent of M rows at once (independent chains, interleaved): for
-// every row j, the largest thr[j] with at least R of key[j][..] >= thr[j],
-// resolved from bit top down to bit stop.  thr[j] enters holding the row's
-// common key prefix; a bit inside a row's prefix leaves its thr unchanged
-// (every key has it, or none), so all rows descend from the highest top.
-// Empty entries hold key 0 and never count (every candidate is >= 1).
+// every row j in the mask open, the largest thr[j] with at least R of
+// key[j][..] >= thr[j], resolved from bit top down.  thr[j] enters holding
+// the row's common key prefix; a bit inside a row's prefix leaves its thr
+// unchanged (every key has it, or none), so all rows descend from the
+// highest top.  A row leaves the descent once exactly R keys are >= its
+// candidate: that candidate is then the answer (fewer steps than bits on
+// distinct scores).  Empty entries hold key 0 and never count (every
+// candidate is >= 1).
 template <int M, int S>
 __device__ __forceinline__ void descend(const uint32_t (&key)[M][S], uint32_t (&thr)[M], int R, int top,
-                                        int stop) {
-  for (int bit = top; bit >= stop; --bit) {
+                                        uint32_t open) {
+  for (int bit = top; bit >= 0 && open != 0u; --bit) {
 #pragma unroll
     for (int j = 0; j < M; ++j) {
-      const uint32_t cand = thr[j] | (1u << bit);
-      int cnt = 0;
+      if ((open >> j) & 1u) {
+        const uint32_t cand = thr[j] | (1u << bit);
+        int cnt = 0;
 #pragma unroll
-      for (int sl = 0; sl < S; ++sl) cnt += (int)__popcll(__ballot(key[j][sl] >= cand));
-      thr[j] = cnt >= R ? cand : thr[j];
+        for (int sl = 0; sl < S; ++sl) cnt += (int)__popcll(__ballot(key[j][sl] >= cand));
+        if (cnt >= R) {
+          thr[j] = cand;
+          if (cnt == R) open &= ~(1u << j);
+        }
+      }
     }
   }
 }
@@ -281,213 +294,254 @@ template <int D, bool QUEST, bool GIVEN>
 __device__ void two_pass_rows(const RowParams& P, unsigned char* s_dyn, uint32_t* s_bits, uint32_t* s_small,
                               const uint16_t* mhead, const uint16_t* qtile, size_t rowbase, int nc, int R,
                               int w, int lane) {
-  using G = RowGeo<D>;
-  constexpr int KD = QUEST ? 2 * D : D;
-  constexpr int KS = G::KS, RT = G::RT, RG = G::RG;
-  constexpr int KB = QUEST ? 2 * KS : KS;
-  uint16_t* s_q = reinterpret_cast<uint16_t*>(s_dyn);                     // [RG][QP] staged queries
-  uint32_t* s_qidx = reinterpret_cast<uint32_t*>(s_dyn + G::kQBytes);     // [RT][KS][64]  Quest indices
-  unsigned char* s_r = s_dyn + G::kQBytes + G::kIdxBytes;
-  uint32_t* s_max = reinterpret_cast<uint32_t*>(s_r);                     // [RG][kStreams] pass 1
-  uint64_t* s_list = reinterpret_cast<uint64_t*>(s_r);                    // [RG][kCap]     pass 2, 3
+  using C = RowChunk<D, QUEST>;
+  constexpr int KS = D / 32;   // k-steps of 32 channels (raw query rows)
+  uint32_t* s_max = reinterpret_cast<uint32_t*>(s_dyn);                   // [64][kBoundVals] after pass 1
+  uint64_t* s_list = reinterpret_cast<uint64_t*>(s_dyn + kRegionA);       // [64][kCap]
   uint32_t* s_cnt = s_small;            // [64] list lengths
   uint32_t* s_bound = s_small + 64;     // [64] bound keys L
   uint32_t* s_over = s_small + 128;     // [2]  overflowed rows (bit mask)
-  float* s_fbound = reinterpret_cast<float*>(s_small + 132);  // [64] bounds as scores (16-byte aligned)
+  float* s_fbound = reinterpret_cast<float*>(s_small + 132);  // [64] bounds as scores
   const int g = lane >> 4, c16 = lane & 15;
-  const int nchunks = (nc + 15) / 16;
+  const int rt = w & 3, qd = w >> 2;   // this wave: row tile rt, column tile qd of every super-chunk
+  const int nsc = (nc + C::kBlocks - 1) / C::kBlocks;
   const int NB = P.s.NB;
 
-  for (int row0 = 0; row0 < kBlock; row0 += RG) {
-    if constexpr (!GIVEN) {
-      const uint16_t* src = qtile + (size_t)row0 * D;
-      for (int i = threadIdx.x; i < RG * D / 8; i += 64 * kRowWaves) {
-        const int r = i / (D / 8), c = i % (D / 8);
-        *reinterpret_cast<uint4*>(s_q + r * G::QP + 8 * c) = *reinterpret_cast<const uint4*>(src + (size_t)r * D + 8 * c);
+  if (threadIdx.x < kBlock) s_cnt[threadIdx.x] = 0u;
+
+  // ---- A operand: rows 16 rt + c16, raw; Quest adds the 2:4 indices --------
+  bf16x8 a[GIVEN ? 1 : KS];
+  uint32_t qidx[(QUEST && !GIVEN) ? KS : 1];
+  if constexpr (!GIVEN) {
+    const uint16_t* qrow = qtile + (size_t)(16 * rt + c16) * D;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g);
+      a[ks] = as_bf16x8(v);
+      if constexpr (QUEST) qidx[ks] = quest_index(v);
+    }
+    wait_vmcnt<0>();  // Q in registers: the loop's vmcnt waits count ring loads only
+  }
+  const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(s_dyn));
+  // this wave's 1 KiB loads of super-chunk sc: i = w, w + 16, ... < kLoads;
+  // rows past the last candidate re-read the super-chunk's first row (block
+  // 1 + 64 sc <= nc for every super-chunk issued)
+  auto issue = [&](int sc) {
+    const uint32_t slot = ring_lds + (uint32_t)((sc % C::kRing) * C::kBytes);
+    const uint16_t* base = mhead + (size_t)__builtin_amdgcn_readfirstlane(1 + C::kBlocks * sc) * C::KD;
+#pragma unroll
+    for (int j = 0; j < C::kPerWave; ++j) {
+      const int i = w + kRowWaves * j;
+      if (i < C::kLoads) {
+        const int p16 = i * 64 + lane;  // 16-byte unit of the slot
+        const int r = p16 / C::CPR;
+        const int col = (p16 % C::CPR) ^ (r & C::SWZ);
+        const int rr = (C::kBlocks * sc + r < nc) ? r : 0;
+        dma16(base, (uint32_t)((rr * C::KD + col * 8) * 2), __builtin_amdgcn_readfirstlane(slot + i * 1024));
       }
     }
-    if (threadIdx.x < RG) s_cnt[threadIdx.x] = 0u;
-    __syncthreads();
-
-    // A operand of tile rt, k-step ks: row 16 rt + c16, channels 32 ks + 8 g ..
-    // (z: an opaque zero per chunk, so the loads are not hoisted out of the
-    // chunk loop into registers the loop cannot spare)
-    auto a_op = [&](int rt, int ks, int z) {
-      return *reinterpret_cast<const uint4*>(s_q + (16 * rt + c16) * G::QP + 32 * ks + 8 * g + z);
-    };
-    if constexpr (QUEST && !GIVEN) {
-      {
-        if (threadIdx.x < RT * KS * 64) {
-          const int ln = threadIdx.x & 63, rk = threadIdx.x >> 6;  // rk = KS rt + ks
-          const int rt = rk / KS, ks = rk % KS;
-          s_qidx[threadIdx.x] = quest_index(*reinterpret_cast<const uint4*>(
-              s_q + (16 * rt + (ln & 15)) * G::QP + 32 * ks + 8 * (ln >> 4)));
+  };
+  // scores of super-chunk sc for this wave: rows 16 rt + 4 g + i, column
+  // 16 qd + c16 (candidate p = 64 sc + 16 qd + c16, block 1 + p)
+  auto scores = [&](int sc, f32x4& acc) {
+    const int p = C::kBlocks * sc + 16 * qd + c16;
+    if constexpr (GIVEN) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        acc[i] = p < nc ? P.row_scores[(rowbase + 16 * rt + 4 * g + i) * NB + 1 + p] : 0.f;
+    } else {
+      const unsigned char* slot = s_dyn + (sc % C::kRing) * C::kBytes;
+      const int br = 16 * qd + c16;
+      // every B operand of the step read before the first MFMA: one LDS
+      // round trip per step, not one per k-step (the steps are short and
+      // barrier-separated, so their latency is not hidden by other waves)
+      // (in groups of at most 8 operands, 32 registers)
+      constexpr int NBV = QUEST ? 2 * KS : KS;
+      constexpr int GRP = NBV < 8 ? NBV : 8;
+      constexpr int KG = QUEST ? GRP / 2 : GRP;   // k-steps per group
+      acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k0 = 0; k0 < KS; k0 += KG) {
+        uint4 bv[GRP];
+#pragma unroll
+        for (int j = 0; j < GRP; ++j) {
+          const int c = QUEST ? 8 * (k0 + j / 2) + 4 * (j % 2) + g : 4 * (k0 + j) + g;
+          bv[j] = *reinterpret_cast<const uint4*>(slot + C::off(br, c));
         }
-        __syncthreads();
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int kk = 0; kk < KG; ++kk) {
+          const int ks = k0 + kk;
+          if constexpr (QUEST)
+            acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[ks], as_bf16x16(bv[2 * kk], bv[2 * kk + 1]), acc,
+                                                            (int)qidx[ks], 0, 0);
+          else
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks], as_bf16x8(bv[kk]), acc, 0, 0, 0);
+        }
       }
     }
-    // scores of chunk c: lane holds rows 16 rt + 4 g + i of the group, column
-    // c16 (candidate p = 16 c + c16, block 1 + p); entries with p >= nc are
-    // unused (block 1 is read in their place)
-    auto chunk = [&](int c, f32x4 (&acc)[RT]) {
-      const int p = 16 * c + c16;
-      if constexpr (GIVEN) {
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            acc[rt][i] = p < nc ? P.row_scores[(rowbase + row0 + 16 * rt + 4 * g + i) * NB + 1 + p] : 0.f;
-      } else {
-        int z = 0;
-        asm volatile("" : "+v"(z));
-        const uint16_t* mrow = mhead + (size_t)(1 + (p < nc ? p : 0)) * KD;
-        uint4 b[KB];
-#pragma unroll
-        for (int j = 0; j < KB; ++j)
-          b[j] = *reinterpret_cast<const uint4*>(mrow + (QUEST ? 64 * (j / 2) + 32 * (j % 2) + 8 * g : 32 * j + 8 * g));
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-          for (int rt = 0; rt < RT; ++rt) {
-            if constexpr (QUEST)
-              acc[rt] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(as_bf16x8(a_op(rt, ks, z)),
-                                                                  as_bf16x16(b[2 * ks], b[2 * ks + 1]), acc[rt],
-                                                                  (int)s_qidx[(KS * rt + ks) * 64 + lane + z], 0, 0);
-            else
-              acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a_op(rt, ks, z)), as_bf16x8(b[ks]), acc[rt],
-                                                                0, 0, 0);
-          }
-        }
+  };
+  // one pass over the super-chunks: body(sc, acc, in)
+  auto sweep = [&](auto&& body) {
+    if constexpr (GIVEN) {
+      for (int sc = 0; sc < nsc; ++sc) {
+        f32x4 acc;
+        scores(sc, acc);
+        body(acc, C::kBlocks * sc + 16 * qd + c16 < nc, C::kBlocks * sc + 16 * qd + c16);
       }
-    };
-
-    // ---- pass 1: stream maxima ----------------------------------------------
-    {
-      float mx[RT][4];
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) mx[rt][i] = -__builtin_inff();
-      for (int c = w; c < nchunks; c += kRowWaves) {
-        f32x4 acc[RT];
-        chunk(c, acc);
-        const bool in = 16 * c + c16 < nc;
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) mx[rt][i] = fmaxf(mx[rt][i], in ? acc[rt][i] : -__builtin_inff());
+    } else if constexpr (C::kRing == 2) {
+      issue(0);
+      for (int sc = 0; sc < nsc; ++sc) {
+        wait_vmcnt<0>();  // this wave's loads of sc landed
+        lds_barrier();    // everyone's did; everyone is done reading sc - 1's slot
+        if (sc + 1 < nsc) issue(sc + 1);
+        f32x4 acc;
+        scores(sc, acc);
+        body(acc, C::kBlocks * sc + 16 * qd + c16 < nc, C::kBlocks * sc + 16 * qd + c16);
       }
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          s_max[(16 * rt + 4 * g + i) * kStreams + 16 * w + c16] =
-              mx[rt][i] == -__builtin_inff() ? 0u : order_key(mx[rt][i]);
+    } else {
+      for (int sc = 0; sc < nsc; ++sc) {
+        issue(sc);
+        wait_vmcnt<0>();
+        lds_barrier();
+        f32x4 acc;
+        scores(sc, acc);
+        body(acc, C::kBlocks * sc + 16 * qd + c16 < nc, C::kBlocks * sc + 16 * qd + c16);
+        wait_lgkm0();
+        lds_barrier();    // the slot is free for the next issue
+      }
     }
-    __syncthreads();
+    wait_lgkm0();
+    __syncthreads();      // the ring's last reads are done: its space is reused
+  };
 
-    // ---- bounds: wave w, rows RT w + j ---------------------------------------
-    {
-      uint32_t key[RT][kStreams / 64], thr[RT];
-      int top = -1;
+  // ---- pass 1: the four largest scores of every (row, stream) --------------
+  {
+    float top[4][kTop];
 #pragma unroll
-      for (int j = 0; j < RT; ++j) {
-        uint32_t hi = 0u, lo = 0xffffffffu;
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int sl = 0; sl < kStreams / 64; ++sl) {
-          key[j][sl] = s_max[(RT * w + j) * kStreams + 64 * sl + lane];
-          hi = max(hi, key[j][sl]);
-          lo = min(lo, key[j][sl] == 0u ? 0xffffffffu : key[j][sl]);
+      for (int j = 0; j < kTop; ++j) top[i][j] = -__builtin_inff();
+    sweep([&](const f32x4& acc, bool in, int) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        // insertion into the sorted four (top[0] >= .. >= top[3]), each new
+        // entry from the old ones: new top[j] = med3(top[j - 1], top[j], x)
+        const float x = in ? acc[i] : -__builtin_inff();
+        float nt[kTop];
+        nt[0] = __builtin_amdgcn_fmed3f(top[i][0], x, __builtin_inff());
+#pragma unroll
+        for (int j = 1; j < kTop; ++j) nt[j] = __builtin_amdgcn_fmed3f(top[i][j - 1], top[i][j], x);
+#pragma unroll
+        for (int j = 0; j < kTop; ++j) top[i][j] = nt[j];
+      }
+    });
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < kTop; ++j)
+        s_max[(16 * rt + 4 * g + i) * kBoundVals + (16 * qd + c16) * kTop + j] =
+            top[i][j] == -__builtin_inff() ? 0u : order_key(top[i][j]);
+  }
+  __syncthreads();
+
+  // ---- bounds: wave w, rows 4 w + j ----------------------------------------
+  {
+    constexpr int SL = kBoundVals / 64;
+    uint32_t key[4][SL], thr[4];
+    int top = -1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t hi = 0u, lo = 0xffffffffu;
+#pragma unroll
+      for (int sl = 0; sl < SL; ++sl) {
+        key[j][sl] = s_max[(4 * w + j) * kBoundVals + 64 * sl + lane];
+        hi = max(hi, key[j][sl]);
+        lo = min(lo, key[j][sl] == 0u ? 0xffffffffu : key[j][sl]);
+      }
+      int tj;
+      thr[j] = key_prefix(wave_min_key(lo), wave_max_key(hi), &tj);
+      top = tj > top ? tj : top;
+    }
+    descend<4, SL>(key, thr, R, top, 0xfu);
+    if (lane == 0) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        s_bound[4 * w + j] = thr[j];
+        s_fbound[4 * w + j] = bound_value(thr[j]);
+      }
+    }
+  }
+  __syncthreads();  // the stream values are read: the ring takes their space again
+
+  // ---- pass 2: lists of the scores >= L ------------------------------------
+  {
+    const float4 fb = *reinterpret_cast<const float4*>(s_fbound + 16 * rt + 4 * g);
+    const float fl[4] = {fb.x, fb.y, fb.z, fb.w};
+    sweep([&](const f32x4& acc, bool in, int p) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (in && acc[i] >= fl[i]) {
+          const int r = 16 * rt + 4 * g + i;
+          const uint32_t at = atomicAdd(&s_cnt[r], 1u);
+          if (at < (uint32_t)kCap) s_list[r * kCap + at] = ((uint64_t)order_key(acc[i]) << 32) | (uint32_t)p;
         }
-        int tj;
+      }
+    });
+  }
+
+  // ---- pass 3: exact top R of each list ------------------------------------
+  {
+    constexpr int SL = (kCap + 63) / 64;
+    uint32_t key[4][SL], pos[4][SL], thr[4];
+    int n[4];
+    int top = -1;
+    uint32_t open = 0u;   // rows whose lists need the descent
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = 4 * w + j;
+      n[j] = __builtin_amdgcn_readfirstlane((int)s_cnt[r]);
+      // a list shorter than R cannot happen (pass 2 recomputes pass 1's
+      // scores exactly); it is sent to the quarter form like an overflow
+      const bool ok = n[j] >= R && n[j] <= kCap;
+      uint32_t hi = 0u, lo = 0xffffffffu;
+#pragma unroll
+      for (int sl = 0; sl < SL; ++sl) {
+        const int e = 64 * sl + lane;
+        const uint64_t v = (ok && e < n[j]) ? s_list[r * kCap + e] : 0ull;
+        key[j][sl] = (uint32_t)(v >> 32);
+        pos[j][sl] = (uint32_t)v;
+        hi = max(hi, key[j][sl]);
+        lo = min(lo, key[j][sl] == 0u ? 0xffffffffu : key[j][sl]);
+      }
+      int tj = -1;
+      thr[j] = 0u;
+      if (ok && n[j] > R) {  // a list of exactly R is kept whole
         thr[j] = key_prefix(wave_min_key(lo), wave_max_key(hi), &tj);
-        top = tj > top ? tj : top;
+        open |= 1u << j;
+      } else if (!ok && lane == 0) {
+        atomicOr(&s_over[r >> 5], 1u << (r & 31));
       }
-      descend<RT, kStreams / 64>(key, thr, R, top, 0);
-      if (lane == 0) {
-#pragma unroll
-        for (int j = 0; j < RT; ++j) s_bound[RT * w + j] = thr[j];
-      }
+      n[j] = ok ? n[j] : 0;
+      top = tj > top ? tj : top;
     }
-    __syncthreads();  // the stream maxima are read: the lists take their space
-
-    // ---- pass 2: lists of the scores >= L ------------------------------------
-    {
-      if (threadIdx.x < RG) s_fbound[threadIdx.x] = bound_value(s_bound[threadIdx.x]);
-      __syncthreads();
-      for (int c = w; c < nchunks; c += kRowWaves) {
-        f32x4 acc[RT];
-        chunk(c, acc);
-        const int p = 16 * c + c16;
-        if (p < nc) {
+    descend<4, SL>(key, thr, R, top, open);
 #pragma unroll
-          for (int rt = 0; rt < RT; ++rt) {
-            // the bounds of rows 16 rt + 4 g .. + 3, re-read per chunk (not
-            // held across the loop: registers)
-            const float4 fb = *reinterpret_cast<const float4*>(s_fbound + 16 * rt + 4 * g);
-            const float fl[4] = {fb.x, fb.y, fb.z, fb.w};
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              if (acc[rt][i] >= fl[i]) {
-                const int r = 16 * rt + 4 * g + i;
-                const uint32_t at = atomicAdd(&s_cnt[r], 1u);
-                if (at < (uint32_t)kCap) s_list[r * kCap + at] = ((uint64_t)order_key(acc[rt][i]) << 32) | (uint32_t)p;
-              }
-            }
-          }
-        }
-      }
-    }
-    __syncthreads();
-
-    // ---- pass 3: exact top R of each list ------------------------------------
-    {
-      constexpr int SL = kCap / 64;
-      uint32_t key[RT][SL], pos[RT][SL], thr[RT];
-      int n[RT];
-      int top = -1;
-#pragma unroll
-      for (int j = 0; j < RT; ++j) {
-        const int r = RT * w + j;
-        n[j] = __builtin_amdgcn_readfirstlane((int)s_cnt[r]);
-        // a list shorter than R cannot happen (pass 2 recomputes pass 1's
-        // scores exactly); it is sent to the quarter form like an overflow
-        const bool ok = n[j] >= R && n[j] <= kCap;
-        uint32_t hi = 0u, lo = 0xffffffffu;
-#pragma unroll
-        for (int sl = 0; sl < SL; ++sl) {
-          const int e = 64 * sl + lane;
-          const uint64_t v = (ok && e < n[j]) ? s_list[r * kCap + e] : 0ull;
-          key[j][sl] = (uint32_t)(v >> 32);
-          pos[j][sl] = (uint32_t)v;
-          hi = max(hi, key[j][sl]);
-          lo = min(lo, key[j][sl] == 0u ? 0xffffffffu : key[j][sl]);
-        }
-        int tj = -1;
-        thr[j] = 0u;
-        if (ok) {
-          thr[j] = key_prefix(wave_min_key(lo), wave_max_key(hi), &tj);
-        } else if (lane == 0) {
-          atomicOr(&s_over[(row0 + r) >> 5], 1u << ((row0 + r) & 31));
-        }
-        n[j] = ok ? n[j] : 0;
-        top = tj > top ? tj : top;
-      }
-      descend<RT, SL>(key, thr, R, top, 0);
-#pragma unroll
-      for (int j = 0; j < RT; ++j) {
-        if (n[j] == 0) continue;
+    for (int j = 0; j < 4; ++j) {
+      if (n[j] == 0) continue;
+      uint32_t last = 0xffffffffu;  // keys == thr kept up to this position
+      uint32_t t = thr[j];
+      if (n[j] == R) {
+        t = 0u;  // every entry (keys are >= 1)
+      } else {
         int above = 0, eq = 0;
 #pragma unroll
         for (int sl = 0; sl < SL; ++sl) {
-          above += (int)__popcll(__ballot(key[j][sl] > thr[j]));
-          eq += (int)__popcll(__ballot(key[j][sl] == thr[j]));
+          above += (int)__popcll(__ballot(key[j][sl] > t));
+          eq += (int)__popcll(__ballot(key[j][sl] == t));
         }
         // the keys equal to thr are taken lowest position first: the need-th
         // smallest of their positions (positions < 2048) by a radix descent
-        uint32_t last = 0xffffffffu;
         if (above + eq > R) {
           const int need = R - above;
           uint32_t lo = 0u;
@@ -495,22 +549,24 @@ __device__ void two_pass_rows(const RowParams& P, unsigned char* s_dyn, uint32_t
             int c = 0;
 #pragma unroll
             for (int sl = 0; sl < SL; ++sl)
-              c += (int)__popcll(__ballot(key[j][sl] == thr[j] && pos[j][sl] < lo + (1u << bit)));
+              c += (int)__popcll(__ballot(key[j][sl] == t && pos[j][sl] < lo + (1u << bit)));
             if (c < need) lo += 1u << bit;
           }
           last = lo;
         }
+      }
 #pragma unroll
-        for (int sl = 0; sl < SL; ++sl) {
-          if (key[j][sl] > thr[j] || (key[j][sl] == thr[j] && pos[j][sl] <= last)) {
-            const int blk = 1 + (int)pos[j][sl];
-            atomicOr(&s_bits[blk >> 5], 1u << (blk & 31));
-          }
+      for (int sl = 0; sl < SL; ++sl) {
+        const bool take = n[j] == R ? key[j][sl] != 0u
+                                    : (key[j][sl] > t || (key[j][sl] == t && pos[j][sl] <= last));
+        if (take) {
+          const int blk = 1 + (int)pos[j][sl];
+          atomicOr(&s_bits[blk >> 5], 1u << (blk & 31));
         }
       }
     }
-    __syncthreads();  // the lists and queries are rewritten by the next group
   }
+  __syncthreads();
 }
 
 // GIVEN: the scores come from P.row_scores (D and QUEST then unused)
@@ -568,7 +624,7 @@ __global__ void __launch_bounds__(64 * kRowWaves) rowsel_kernel(RowParams P) {
 
 template <int D, bool QUEST, bool GIVEN>
 hipError_t launch_rows(RowParams P, hipStream_t stream) {
-  const size_t smem = std::max(sizeof(float) * (size_t)kQuarter * P.pitch, RowGeo<D>::kBytes);
+  const size_t smem = std::max(sizeof(float) * (size_t)kQuarter * P.pitch, kTwoPassBytes);
   const size_t fixed = sizeof(uint32_t) * (UGBS_MAX_BLOCKS_ROWS / 32 + 196);
   if (smem + fixed > 65536) {
     const hipError_t e = hipFuncSetAttribute((const void*)rowsel_kernel<D, QUEST, GIVEN>,
