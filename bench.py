@@ -387,11 +387,13 @@ def main():
     layer, f_sc, f_att = layer_record(w, ms_per_step, stage_avg, kv, trig, inp.needles)
     f_dense = 4.0 * w.d * w.B * w.H * (w.N * (w.N + 1) / 2)
 
-    graph = fused = rows = None
+    graph = fused = rows = quest_forms = None
     if not a.no_variants:
         graph = run_graph(torch, dev, step, O, stream, a)
         fused = run_fused(torch, dev, ugbs, p, Q, K, V, O, stream, a, f_att)
         rows = run_rows(torch, dev, ugbs, w, p, Q, K, V, stream, a, inp.needles)
+        if w.backbone == ugbs.QUEST:
+            quest_forms = run_quest_forms(torch, dev, ugbs, w, p, Q, bufs, stream, a)
 
     cold = None
     if not a.no_cold:
@@ -496,6 +498,7 @@ def main():
         "selection": layer["selection"],
         "fused_selection": fused,
         "row_selection": rows,
+        "quest_scoring_forms": quest_forms,
         "ms_per_step_median": round(float(np.median(step_ms)), 4),
         "graph_replay": graph,
         "cold": cold,
@@ -571,6 +574,51 @@ def run_fused(torch, dev, ugbs, p, Q, K, V, O, stream, a, f_att):
                           "route_flags": round(float(fst[2]), 4), "attend_select": round(float(fst[3]), 4)},
             "attend_select_TFLOPs": round(f_att / (fst[3] * 1e-3) / 1e12, 2),
             "output_identical": same}
+
+
+def run_quest_forms(torch, dev, ugbs, w, p, Q, bufs, stream, a):
+    """Quest tile scores in both forms, each into a full [B, H, T, N_B] tensor:
+    the per-channel vector-ALU form (one bf16 dot2 per bound term) and the
+    2:4-sparse matrix-core form inside ugbs_score_select (which also runs the
+    selection; the selection alone is timed from the same scores through
+    scores_in, so the matrix-core scoring time is the difference)."""
+    so_v = torch.empty((w.B, w.H, w.T, w.NB), dtype=torch.float32, device=dev)
+    so_m = torch.empty_like(so_v)
+    idx = torch.empty_like(bufs.idx_sorted)
+    sig = torch.empty_like(bufs.sigma)
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize(dev)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record(stream)
+        for _ in range(reps):
+            fn()
+        ev[1].record(stream)
+        torch.cuda.synchronize(dev)
+        return ev[0].elapsed_time(ev[1]) / reps
+
+    reps = max(2, a.steps // 2)
+    ms_valu = timed(lambda: ugbs.ugbs_quest_scores_valu(p, Q, bufs.meta, so_v), reps)
+    ms_mfma_sel = timed(lambda: ugbs.ugbs_score_select(p, Q, bufs.meta, idx, sig, scores_out=so_m), reps)
+    ms_sel = timed(lambda: ugbs.ugbs_score_select(p, Q, bufs.meta, idx, sig, scores_in=so_m), reps)
+    fin = torch.isfinite(so_m)
+    same_inf = bool(torch.equal(fin, torch.isfinite(so_v)))
+    rel = float(((so_v - so_m).abs()[fin] / so_m.abs()[fin].clamp_min(1e-30)).max())
+    # bound terms: d per (row, candidate block); one dot2 instruction lane-op each
+    terms = float(w.B * w.H) * sum(max(t - 1, 0) for t in range(w.T)) * 64 * w.d
+    valu_peak = 256 * 64 * 2.4e9          # lane-ops per second: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+    rec = {"valu_dot2_ms": round(ms_valu, 4),
+           "mfma_score_plus_select_ms": round(ms_mfma_sel, 4),
+           "select_only_ms": round(ms_sel, 4),
+           "mfma_score_ms": round(ms_mfma_sel - ms_sel, 4),
+           "valu_over_mfma": round(ms_valu / max(ms_mfma_sel - ms_sel, 1e-9), 2),
+           "bound_terms": terms,
+           "valu_frac_of_dot2_peak": round(terms / (ms_valu * 1e-3) / valu_peak, 4),
+           "same_inf_pattern": same_inf, "max_rel_diff": rel}
+    log(f"quest forms: {rec}")
+    del so_v, so_m, idx, sig
+    return rec
 
 
 def run_rows(torch, dev, ugbs, w, p, Q, K, V, stream, a, needles):

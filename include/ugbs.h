@@ -69,7 +69,7 @@ extern "C" {
 #define UGBS_API
 #endif
 
-#define UGBS_ABI_VERSION 9
+#define UGBS_ABI_VERSION 10
 #define UGBS_BLOCK 64          /* BLOCK_M = BLOCK_N = 64 tokens (Section 3.1, 3.2) */
 #define UGBS_MAX_BLOCKS 4096   /* N_B <= 4096, i.e. N <= 262144 */
 #define UGBS_MAX_BLOCKS_ROWS 2048 /* ugbs_select_rows, ugbs_bai_tiles, ugbs_bai_heads: N_B <= 2048 */
@@ -198,6 +198,23 @@ UGBS_API int ugbs_score_select(const ugbs_problem* p, const void* Q, const void*
 UGBS_API int ugbs_route(const ugbs_problem* p, const float* sigma, const int32_t* idx_sorted,
                int32_t* kv_idx, float* sigma_bar, float* tau, uint8_t* trigger,
                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Quest tile scores on the vector ALU (A.2-A.3 with Eq. (quest-score)), the
+ * literal per-channel form, kept for comparison with the matrix-core
+ * contraction inside ugbs_score_select (UGBS_QUEST only, else
+ * UGBS_ERR_BACKBONE).  For channel c the bound term max(q_c kmax_c,
+ * q_c kmin_c) is one two-element bf16 dot product (min(q_c, 0),
+ * max(q_c, 0)) . (kmin_c, kmax_c), of which one product is zero; the terms
+ * of a row are accumulated in fp32 in channel order and the tile score is
+ * the maximum over the 64 rows.  Both forms sum exact bf16 products in
+ * fp32, so they agree up to the order of the fp32 additions.
+ *   Q          : [B, H, N, d] bf16, 16-byte aligned.
+ *   meta       : Quest output of ugbs_block_meta for the same problem.
+ *   scores_out : [B, H, T, N_B] fp32, 4-byte aligned, fully written: the
+ *                tile score of every candidate of C(t) = {1..t-1}, -inf
+ *                elsewhere (the layout of ugbs_score_select's scores_out). */
+UGBS_API int ugbs_quest_scores_valu(const ugbs_problem* p, const void* Q, const void* meta,
+                                    float* scores_out, void* stream);
 
 /* Stage 4 for callers that cannot allocate device memory (code under HIP
  * graph capture, tight serving loops, harnesses that forbid allocation):

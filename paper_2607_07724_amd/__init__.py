@@ -23,6 +23,7 @@ __all__ = [
     "ugbs_attend_select", "prefill_fused", "ugbs_select_rows", "ugbs_attend_bitmap",
     "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads", "BAI_TILE_FIELDS", "BAI_HEAD_FIELDS",
     "bai_tile_records", "bai_head_records", "ugbs_route_noalloc", "ROUTE_SCRATCH_BYTES",
+    "ugbs_quest_scores_valu",
 ]
 
 KMEAN, QUEST = 0, 1
@@ -116,9 +117,11 @@ def lib():
         L.ugbs_noise_scale.argtypes = [pp, P, P, P, P, P]
         L.ugbs_bai_tiles.argtypes = [pp, P, P, P, ctypes.c_int32, P, P]
         L.ugbs_bai_heads.argtypes = [pp, P, P, ctypes.c_int32, P, P]
+        L.ugbs_quest_scores_valu.argtypes = [pp, P, P, P, P]
         for f in ("ugbs_block_meta", "ugbs_score_select", "ugbs_route", "ugbs_attend", "ugbs_abi_version",
                   "ugbs_attend_select", "ugbs_select_rows", "ugbs_attend_bitmap",
-                  "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads", "ugbs_route_noalloc"):
+                  "ugbs_noise_scale", "ugbs_bai_tiles", "ugbs_bai_heads", "ugbs_route_noalloc",
+                  "ugbs_quest_scores_valu"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -206,6 +209,19 @@ def ugbs_score_select(p: Problem, Q, meta, idx_sorted, sigma, scores_in=None, sc
         nbytes = workspace.numel() * workspace.element_size()
     _raise("ugbs_score_select",
            lib().ugbs_score_select(ctypes.byref(p), q, m, si, so, ix, sg, ws, nbytes, _stream(stream)))
+
+
+def ugbs_quest_scores_valu(p: Problem, Q, meta, scores_out, stream=None):
+    """Quest tile scores on the vector ALU (the literal per-channel form of
+    Eq. (quest-score)): scores_out [B,H,T,N_B] fp32, -inf outside C(t)."""
+    import torch
+    bf = _bf16()
+    dev = Q.device
+    q = _check("Q", Q, (p.batch, p.n_heads, p.seq_len, p.head_dim), bf)
+    m = _check("meta", meta, (p.batch, p.n_kv_heads, p.NB, p.head_dim, p.meta_width), bf, dev)
+    so = _check("scores_out", scores_out, (p.batch, p.n_heads, p.T, p.NB), (torch.float32,), dev)
+    _raise("ugbs_quest_scores_valu",
+           lib().ugbs_quest_scores_valu(ctypes.byref(p), q, m, so, _stream(stream)))
 
 
 def ugbs_route(p: Problem, sigma, idx_sorted, kv_idx, workspace, sigma_bar=None, tau=None,

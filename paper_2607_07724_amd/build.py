@@ -29,7 +29,7 @@ LIB = os.path.join(PKG, "libugbs.so")
 ARCH = "gfx950"
 LLVM_BIN = "/opt/rocm/lib/llvm/bin"
 
-SOURCES = ["block_meta.hip", "score_select.hip", "route.hip", "attend.hip", "rowsel.hip", "bai.hip", "abi.hip"]
+SOURCES = ["block_meta.hip", "score_select.hip", "route.hip", "attend.hip", "rowsel.hip", "bai.hip", "quest_valu.hip", "abi.hip"]
 
 CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

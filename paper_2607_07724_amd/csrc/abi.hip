@@ -117,6 +117,18 @@ int ugbs_score_select(const ugbs_problem* p, const void* Q, const void* meta,
       static_cast<hipStream_t>(stream)));
 }
 
+int ugbs_quest_scores_valu(const ugbs_problem* p, const void* Q, const void* meta, float* scores_out,
+                           void* stream) {
+  Shape s;
+  int st = make_shape(p, &s);
+  if (st) return st;
+  if (s.backbone != UGBS_QUEST) return UGBS_ERR_BACKBONE;
+  if (!Q || !meta || !scores_out) return UGBS_ERR_NULL;
+  if (!aligned(Q, 16) || !aligned(meta, 16) || !aligned(scores_out, 4)) return UGBS_ERR_ALIGN;
+  return hip_status(ugbs::launch_quest_valu(s, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(meta),
+                                            scores_out, static_cast<hipStream_t>(stream)));
+}
+
 int ugbs_route(const ugbs_problem* p, const float* sigma, const int32_t* idx_sorted,
                int32_t* kv_idx, float* sigma_bar, float* tau, uint8_t* trigger,
                void* workspace, size_t workspace_bytes, void* stream) {

@@ -29,6 +29,10 @@ hipError_t launch_score_select(const Shape& s, const uint16_t* Q, const uint16_t
                                const float* scores_in, float* scores_out,
                                int32_t* idx_sorted, float* sigma, void* workspace,
                                hipStream_t stream);
+// Quest tile scores on the vector ALU (the literal per-channel form), into a
+// [B, H, T, N_B] fp32 tensor.
+hipError_t launch_quest_valu(const Shape& s, const uint16_t* Q, const uint16_t* meta, float* scores_out,
+                             hipStream_t stream);
 // Bytes of packed candidate scores the score kernel writes into the workspace
 // when the caller supplies neither scores_in nor scores_out.
 size_t score_scratch_bytes(const Shape& s);

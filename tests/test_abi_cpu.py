@@ -111,6 +111,26 @@ def test_invalid_problem_rejected_by_every_entry_point(kw, code):
     assert L.ugbs_noise_scale(ctypes.byref(p), fake, fake, fake, fake, None) == want
     assert L.ugbs_bai_tiles(ctypes.byref(p), fake, fake, fake, 4, fake, None) == want
     assert L.ugbs_bai_heads(ctypes.byref(p), fake, fake, 4, fake, None) == want
+    assert L.ugbs_quest_scores_valu(ctypes.byref(p), fake, fake, fake, None) == want
+
+
+def test_quest_scores_valu_checks():
+    """The vector-ALU Quest scoring takes Quest problems only, and rejects
+    missing or misaligned buffers before any launch."""
+    L = ugbs.lib()
+    fake = ctypes.c_void_p(0x100000)
+    km = good(backbone=ugbs.KMEAN)
+    assert L.ugbs_quest_scores_valu(ctypes.byref(km), fake, fake, fake, None) == _enum("UGBS_ERR_BACKBONE")
+    p = good(backbone=ugbs.QUEST)
+    ERR_NULL, ERR_ALIGN = _enum("UGBS_ERR_NULL"), _enum("UGBS_ERR_ALIGN")
+    assert L.ugbs_quest_scores_valu(None, fake, fake, fake, None) == ERR_NULL
+    for i in range(3):
+        args = [fake] * 3
+        args[i] = None
+        assert L.ugbs_quest_scores_valu(ctypes.byref(p), *args, None) == ERR_NULL
+    assert L.ugbs_quest_scores_valu(ctypes.byref(p), ctypes.c_void_p(0x100008), fake, fake, None) == ERR_ALIGN
+    assert L.ugbs_quest_scores_valu(ctypes.byref(p), fake, ctypes.c_void_p(0x100008), fake, None) == ERR_ALIGN
+    assert L.ugbs_quest_scores_valu(ctypes.byref(p), fake, fake, ctypes.c_void_p(0x100002), None) == ERR_ALIGN
 
 
 def test_null_problem_and_null_pointers():
