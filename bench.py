@@ -444,6 +444,8 @@ def main():
         log(f"measured peaks: {probe}")
         roofline["measured_peak_TFLOPs"] = probe["gemm_bf16_TFLOPs"]
         roofline["frac_of_measured_peak"] = round(roofline["achieved"] / probe["gemm_bf16_TFLOPs"], 4)
+        roofline["mfma_loop_TFLOPs"] = probe["mfma_loop_bf16_TFLOPs"]
+        roofline["frac_of_mfma_loop"] = round(roofline["achieved"] / probe["mfma_loop_bf16_TFLOPs"], 4)
 
     # GPU outputs of the units the CPU leg samples, copied before the big legs free memory
     cpu = None
@@ -839,8 +841,39 @@ def measured_peaks(torch, dev, stream):
     torch.cuda.synchronize(dev)
     gemm = 10 * 2.0 * n ** 3 / (e0.elapsed_time(e1) * 1e-3) / 1e12
     del A, B, C
-    return {"copy_GBps": round(copy_gbps, 1), "gemm_bf16_TFLOPs": round(gemm, 1),
-            "copy": "torch elementwise add, 1 GiB in + 1 GiB out", "gemm": "torch.matmul bf16 8192^3"}
+    loops = mfma_loop_peaks(torch, dev, stream)
+    return {"copy_GBps": round(copy_gbps, 1), "gemm_bf16_TFLOPs": round(gemm, 1), **loops,
+            "copy": "torch elementwise add, 1 GiB in + 1 GiB out", "gemm": "torch.matmul bf16 8192^3",
+            "mfma_loop": "libugbs_probe: 2048 workgroups x 4 waves, back-to-back 16x16x32 bf16 MFMA "
+                         "(dense) or 16x16x64 bf16 2:4-sparse MFMA (dense-equivalent FLOP) on 8 "
+                         "accumulator chains per wave, operands toggling every iteration"}
+
+
+def mfma_loop_peaks(torch, dev, stream, n_wg=2048, iters=4000, reps=5):
+    """Matrix-core ceilings of this GPU under a sustained load: TFLOP/s of a
+    tight loop of dense and of 2:4-sparse bf16 matrix instructions."""
+    import ctypes
+    from paper_2607_07724_amd import build
+    L = ctypes.CDLL(build.PROBE_LIB)
+    L.ugbs_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    L.ugbs_probe_flop.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    L.ugbs_probe_flop.restype = ctypes.c_double
+    L.ugbs_probe_out_floats.argtypes = [ctypes.c_int]
+    out = torch.empty(L.ugbs_probe_out_floats(n_wg), dtype=torch.float32, device=dev)
+    st = ctypes.c_void_p(stream.cuda_stream)
+    res = {}
+    for kind, key in ((0, "mfma_loop_bf16_TFLOPs"), (1, "smfmac_loop_bf16_TFLOPs")):
+        assert L.ugbs_probe_mfma(kind, n_wg, iters, ctypes.c_void_p(out.data_ptr()), st) == 0
+        torch.cuda.synchronize(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            assert L.ugbs_probe_mfma(kind, n_wg, iters, ctypes.c_void_p(out.data_ptr()), st) == 0
+        e1.record(stream)
+        torch.cuda.synchronize(dev)
+        res[key] = round(reps * L.ugbs_probe_flop(kind, n_wg, iters) / (e0.elapsed_time(e1) * 1e-3) / 1e12, 1)
+    del out
+    return res
 
 
 def run_stack(torch, dev, ugbs, synth, steps):

@@ -384,3 +384,29 @@ def test_block_limits_per_entry_point():
     assert L.ugbs_bai_heads(ctypes.byref(p), fake, fake, 4, fake, None) == SHAPE
     p2 = ugbs.Problem.make(1, 8, 2, 64 * 2048, 128, 64, 0.1, ugbs.QUEST)
     assert L.ugbs_select_rows(ctypes.byref(p2), None, None, None, fake, fake, None) == _enum("UGBS_ERR_NULL")
+
+
+def test_probe_library_exports_and_rejects_bad_arguments():
+    """The benchmark's matrix-core probe (libugbs_probe.so, include/ugbs_probe.h)
+    exports what its header declares and rejects invalid arguments before any
+    launch; its FLOP count is 16 instructions x 8 chains per iteration and wave."""
+    from paper_2607_07724_amd import build
+    if not os.path.exists(build.PROBE_LIB):
+        pytest.skip("probe library not built here (run __graft_entry__.build())")
+    txt = open(os.path.join(ROOT, "include", "ugbs_probe.h")).read()
+    names = sorted(set(re.findall(r"UGBS_PROBE_API\s+[\w\s\*]+?\b(ugbs_\w+)\s*\(", txt)))
+    assert names == ["ugbs_probe_flop", "ugbs_probe_mfma", "ugbs_probe_out_floats"]
+    L = ctypes.CDLL(build.PROBE_LIB)
+    for n in names:
+        assert hasattr(L, n), n
+    L.ugbs_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    L.ugbs_probe_flop.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    L.ugbs_probe_flop.restype = ctypes.c_double
+    fake = ctypes.c_void_p(0x100000)
+    assert L.ugbs_probe_mfma(2, 8, 8, fake, None) == 1
+    assert L.ugbs_probe_mfma(0, 0, 8, fake, None) == 1
+    assert L.ugbs_probe_mfma(0, 8, 0, fake, None) == 1
+    assert L.ugbs_probe_mfma(1, 8, 8, None, None) == 1
+    assert L.ugbs_probe_flop(0, 3, 5) == 16 * 16 * 32 * 2 * 16 * 5 * 3 * 4
+    assert L.ugbs_probe_flop(1, 3, 5) == 2 * L.ugbs_probe_flop(0, 3, 5)
+    assert L.ugbs_probe_out_floats(3) == 3 * 256
