@@ -88,21 +88,33 @@ def flops_scores(B: int, H: int, T: int, d: int, backbone: int) -> float:
     return 2.0 * KD * B * H * 64 * cand
 
 
+ATTENTION_SOURCES = ("attend.hip", "attend_common.h", "select_common.h", "ugbs_internal.h")
+
+
+def attention_source_sha256():
+    """SHA-256 over the attention kernel's translation unit and the headers
+    it includes (in a fixed order), the key of the recorded traffic."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in ATTENTION_SOURCES:
+        p = os.path.join(ROOT, "paper_2607_07724_amd", "csrc", name)
+        if os.path.exists(p):
+            with open(p, "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
 def measured_traffic(w, q_override):
     """HBM bytes per attention launch from the committed rocprofv3 counter
     passes (FETCH_SIZE + WRITE_SIZE, each scaled by what the counter reads
     for a streaming kernel of known size), or None when the attention source
     has changed since the counters were taken or the workload differs."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", "traffic.json")
-    src = os.path.join(ROOT, "paper_2607_07724_amd", "csrc", "attend.hip")
     if w.name != "C4" or q_override not in (None, 0.1) or not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f).get("attend_kernel<128>")
-    with open(src, "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()
-    if rec is None or rec.get("source_sha256") != sha:
+    if rec is None or rec.get("source_sha256") != attention_source_sha256():
         return None
     return round(rec["fetch_bytes"] + rec["write_bytes"])
 

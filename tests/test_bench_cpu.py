@@ -55,15 +55,19 @@ def test_traffic_record_is_used_only_for_the_source_it_was_taken_on(tmp_path, mo
     src_dir = tmp_path / "paper_2607_07724_amd" / "csrc"
     src_dir.mkdir(parents=True)
     (src_dir / "attend.hip").write_bytes(b"kernel source A")
-    import hashlib
-    sha = hashlib.sha256(b"kernel source A").hexdigest()
+    (src_dir / "attend_common.h").write_bytes(b"helpers A")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    sha = bench.attention_source_sha256()
     rec = {"attend_kernel<128>": {"source_sha256": sha, "fetch_bytes": 100.4, "write_bytes": 20.2}}
     (tmp_path / "profiles" / "traffic.json").write_text(json.dumps(rec))
-    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     c4 = synth.WORKLOADS["C4"]
     assert bench.measured_traffic(c4, None) == 121
     assert bench.measured_traffic(c4, 0.25) is None               # another workload
     assert bench.measured_traffic(synth.WORKLOADS["C2"], None) is None
+    (src_dir / "attend_common.h").write_bytes(b"helpers B")      # an included header changed since
+    assert bench.measured_traffic(c4, None) is None
+    (src_dir / "attend_common.h").write_bytes(b"helpers A")
+    assert bench.measured_traffic(c4, None) == 121
     (src_dir / "attend.hip").write_bytes(b"kernel source B")      # kernel changed since
     assert bench.measured_traffic(c4, None) is None
 
