@@ -14,9 +14,10 @@
 // and their signs the sparsity indices (quest_index).  Every product is an
 // exact bf16 x bf16 product; sums are fp32.  The wave's 64 raw query rows
 // stay in registers as the A operand (with the indices for Quest).  Metadata
-// rows (the B operand) come in chunks of 16 or 32 blocks that the workgroup's
-// waves fetch together with direct-to-LDS loads into a 4-slot ring (three
-// chunks in flight), so each chunk crosses L2 once per workgroup; in LDS
+// rows (the B operand) come in chunks of 16, 32 or 48 blocks that the
+// workgroup's waves fetch together with direct-to-LDS loads into a ring of 3
+// or 4 slots (two or three chunks in flight), so each chunk crosses L2 once
+// per workgroup; in LDS
 // the 16-byte column c of row r sits at c ^ (r mod 16), which makes the
 // operand reads bank-conflict free.  The max over the tile's rows (A.3) is
 // the max over a lane's 16 accumulators and then across the four 16-lane
@@ -44,7 +45,6 @@ namespace {
 
 constexpr int kMaxGroup = 4;    // sibling query heads per workgroup
 constexpr int kSelWaves = 4;    // units (waves) per selection workgroup
-constexpr int kRing = 4;        // metadata chunk slots (kRing - 1 in flight)
 
 #define LDS_AS __attribute__((address_space(3)))
 
@@ -123,13 +123,17 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const LDS_AS void*)p;
 }
 
-// Blocks per metadata chunk: 32 (two 16-block MFMA column tiles per
-// barrier) where the query tile already holds the kernel at two waves per
-// SIMD (Quest d 128, K-mean d 256), 16 where the second accumulator set
-// would cost a wave (measured: 4-7% faster, 3-4% slower respectively).
+// Blocks per metadata chunk and ring slots (slots - 1 chunks in flight).
+// Where the query tile already holds the kernel at two waves per SIMD, wider
+// chunks amortise the per-chunk barrier: Quest d 128 takes 48 blocks (three
+// 16-block MFMA column tiles, 24 KiB) in a 3-slot ring, which keeps two
+// workgroups per CU (72 KiB each; 32-block chunks in 4 slots were 1.5-3.5%
+// slower), K-mean d 256 32 blocks in 4 slots.  Elsewhere 16 blocks, where
+// a second accumulator set would cost a wave (3-4% slower measured).
 template <int D, bool QUEST>
 struct MetaChunk {
-  static constexpr int kBlocks = ((QUEST && D == 128) || (!QUEST && D == 256)) ? 32 : 16;
+  static constexpr int kBlocks = (QUEST && D == 128) ? 48 : (!QUEST && D == 256) ? 32 : 16;
+  static constexpr int kRingSlots = (QUEST && D == 128) ? 3 : 4;
   static constexpr int KD = QUEST ? 2 * D : D;
   static constexpr int CPR = KD / 8;                   // 16-byte columns per metadata row
   static constexpr int SWZ = (CPR < 16 ? CPR : 16) - 1;
@@ -269,7 +273,7 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
 #pragma unroll
     for (int j = 0; j < kMine; ++j) off0[j] = lane_off(w + 4 * j, 0, false);
     auto issue = [&](int c) {
-      const uint32_t slot = ring_lds + (uint32_t)((c % kRing) * MC::kBytes);
+      const uint32_t slot = ring_lds + (uint32_t)((c % MC::kRingSlots) * MC::kBytes);
       const uint16_t* base = mhead + (size_t)__builtin_amdgcn_readfirstlane(1 + MC::kBlocks * c) * KD;
       const bool last = MC::kBlocks * (c + 1) >= nc_top;   // workgroup-uniform
       if (fast && !last) {
@@ -286,23 +290,56 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
         if (i < MC::kLoads) dma16(base, lane_off(i, c, last), __builtin_amdgcn_readfirstlane(slot + i * 1024));
       }
     };
-    for (int c = 0; c < kRing - 1 && c < nchunks; ++c) issue(c);
+    for (int c = 0; c < MC::kRingSlots - 1 && c < nchunks; ++c) issue(c);
 
     for (int c = 0; c < nchunks; ++c) {
-      const int after = min(kRing - 2, nchunks - 1 - c);  // chunks issued after c
+      const int after = min(MC::kRingSlots - 2, nchunks - 1 - c);  // chunks issued after c
       wait_vmcnt_dyn(n_mine * after);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of chunk c-1 are done
       lds_barrier();                                    // chunk c landed; chunk c-1 is free
-      if (c + kRing - 1 < nchunks) issue(c + kRing - 1);
+      if (c + MC::kRingSlots - 1 < nchunks) issue(c + MC::kRingSlots - 1);
       if (active) {
-        const unsigned char* slot = ring + (c % kRing) * MC::kBytes;
+        const unsigned char* slot = ring + (c % MC::kRingSlots) * MC::kBytes;
+        constexpr int NCT = MC::kBlocks / 16;
+        // Quest d 128 (outside the roughness mode, whose extra registers
+        // would cost a wave): every B operand of the chunk is read first and
+        // the column tiles' matrix instructions interleave (eight independent
+        // accumulator chains), so no LDS read waits between them
+        constexpr bool kAll = QUEST && D == 128 && !ROUGH;
+        f32x4 accs[kAll ? NCT : 1][4];
+        if constexpr (kAll) {
+          bf16x16 bb[NCT][KA];
 #pragma unroll
-        for (int ct = 0; ct < MC::kBlocks / 16; ++ct) {   // 16-block column tiles of the chunk
+          for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+            for (int ks = 0; ks < KA; ++ks) {
+              const int br = 16 * ct + c16;
+              const uint4 b0 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + g));
+              const uint4 b1 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + 4 + g));
+              bb[ct][ks] = as_bf16x16(b0, b1);
+            }
+#pragma unroll
+          for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+            for (int rt = 0; rt < 4; ++rt) accs[ct][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < KA; ++ks)
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+              for (int rt = 0; rt < 4; ++rt)
+                accs[ct][rt] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[rt][ks], bb[ct][ks], accs[ct][rt],
+                                                                         (int)qidx[rt][ks], 0, 0);
+        }
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) {   // 16-block column tiles of the chunk
           const int br = 16 * ct + c16;                  // block row of this lane's column
           f32x4 acc[4];
 #pragma unroll
-          for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if constexpr (QUEST) {
+          for (int rt = 0; rt < 4; ++rt) acc[rt] = kAll ? accs[kAll ? ct : 0][rt] : f32x4{0.f, 0.f, 0.f, 0.f};
+          if constexpr (kAll) {
+            // accumulated above
+          } else if constexpr (QUEST) {
             // sum over the k-step's 32 channels of q * (q > 0 ? kmax : kmin):
             // B holds the (kmin, kmax) pairs of channels 4 g .. 4 g + 3 and
             // 16 + 4 g .. 16 + 4 g + 3 (two 16-byte columns of the row)
@@ -565,7 +602,7 @@ __global__ void __launch_bounds__(64 * kSelWaves) select_kernel(SelParams P) {
 template <int D, bool QUEST, int OUT>
 hipError_t launch_score(SelParams P, hipStream_t stream) {
   using MC = MetaChunk<D, QUEST>;
-  P.ring_lds = kRing * MC::kBytes;
+  P.ring_lds = MC::kRingSlots * MC::kBytes;
   const size_t smem = (size_t)P.ring_lds;
   if (smem > 65536) {
     const hipError_t e = hipFuncSetAttribute((const void*)score_kernel<D, QUEST, OUT>,
