@@ -14,10 +14,10 @@
 // and their signs the sparsity indices (quest_index).  Every product is an
 // exact bf16 x bf16 product; sums are fp32.  The wave's 64 raw query rows
 // stay in registers as the A operand (with the indices for Quest).  Metadata
-// rows (the B operand) come in chunks of 16, 32 or 48 blocks that the
-// workgroup's waves fetch together with direct-to-LDS loads into a ring of 3
-// or 4 slots (two or three chunks in flight), so each chunk crosses L2 once
-// per workgroup; in LDS
+// rows (the B operand) come in chunks of 16 or 32 blocks that the workgroup's
+// waves fetch together with direct-to-LDS loads into a ring of 3 or 4 slots
+// (two or three chunks in flight), so each chunk crosses L2 once per
+// workgroup; in LDS
 // the 16-byte column c of row r sits at c ^ (r mod 16), which makes the
 // operand reads bank-conflict free.  The max over the tile's rows (A.3) is
 // the max over a lane's 16 accumulators and then across the four 16-lane
@@ -123,16 +123,14 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const LDS_AS void*)p;
 }
 
-// Blocks per metadata chunk and ring slots (slots - 1 chunks in flight).
-// Where the query tile already holds the kernel at two waves per SIMD, wider
-// chunks amortise the per-chunk barrier: Quest d 128 takes 48 blocks (three
-// 16-block MFMA column tiles, 24 KiB) in a 3-slot ring, which keeps two
-// workgroups per CU (72 KiB each; 32-block chunks in 4 slots were 1.5-3.5%
-// slower), K-mean d 256 32 blocks in 4 slots.  Elsewhere 16 blocks, where
-// a second accumulator set would cost a wave (3-4% slower measured).
+// Blocks per metadata chunk: 32 (two 16-block MFMA column tiles per
+// barrier) for Quest d 128 and K-mean d 256, 16 elsewhere, where the second
+// accumulator set would cost a wave (measured: 4-7% faster, 3-4% slower
+// respectively).  Ring slots (slots - 1 chunks in flight): 3 for Quest d 128
+// (48 KiB, three workgroups per CU, see score_kernel_q128), 4 elsewhere.
 template <int D, bool QUEST>
 struct MetaChunk {
-  static constexpr int kBlocks = (QUEST && D == 128) ? 48 : (!QUEST && D == 256) ? 32 : 16;
+  static constexpr int kBlocks = ((QUEST && D == 128) || (!QUEST && D == 256)) ? 32 : 16;
   static constexpr int kRingSlots = (QUEST && D == 128) ? 3 : 4;
   static constexpr int KD = QUEST ? 2 * D : D;
   static constexpr int CPR = KD / 8;                   // 16-byte columns per metadata row
@@ -195,7 +193,7 @@ __device__ __forceinline__ float row_diff_sq(const f32x4 (&acc)[4], int lane) {
 }
 
 template <int D, bool QUEST, int OUT>
-__global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
+__device__ __forceinline__ void score_body(const SelParams& P) {
   constexpr bool PACKED = OUT == kOutPacked;
   constexpr bool ROUGH = OUT == kOutRough;
   using MC = MetaChunk<D, QUEST>;
@@ -300,46 +298,13 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
       if (c + MC::kRingSlots - 1 < nchunks) issue(c + MC::kRingSlots - 1);
       if (active) {
         const unsigned char* slot = ring + (c % MC::kRingSlots) * MC::kBytes;
-        constexpr int NCT = MC::kBlocks / 16;
-        // Quest d 128 (outside the roughness mode, whose extra registers
-        // would cost a wave): every B operand of the chunk is read first and
-        // the column tiles' matrix instructions interleave (eight independent
-        // accumulator chains), so no LDS read waits between them
-        constexpr bool kAll = QUEST && D == 128 && !ROUGH;
-        f32x4 accs[kAll ? NCT : 1][4];
-        if constexpr (kAll) {
-          bf16x16 bb[NCT][KA];
 #pragma unroll
-          for (int ct = 0; ct < NCT; ++ct)
-#pragma unroll
-            for (int ks = 0; ks < KA; ++ks) {
-              const int br = 16 * ct + c16;
-              const uint4 b0 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + g));
-              const uint4 b1 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + 4 + g));
-              bb[ct][ks] = as_bf16x16(b0, b1);
-            }
-#pragma unroll
-          for (int ct = 0; ct < NCT; ++ct)
-#pragma unroll
-            for (int rt = 0; rt < 4; ++rt) accs[ct][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int ks = 0; ks < KA; ++ks)
-#pragma unroll
-            for (int ct = 0; ct < NCT; ++ct)
-#pragma unroll
-              for (int rt = 0; rt < 4; ++rt)
-                accs[ct][rt] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[rt][ks], bb[ct][ks], accs[ct][rt],
-                                                                         (int)qidx[rt][ks], 0, 0);
-        }
-#pragma unroll
-        for (int ct = 0; ct < NCT; ++ct) {   // 16-block column tiles of the chunk
+        for (int ct = 0; ct < MC::kBlocks / 16; ++ct) {   // 16-block column tiles of the chunk
           const int br = 16 * ct + c16;                  // block row of this lane's column
           f32x4 acc[4];
 #pragma unroll
-          for (int rt = 0; rt < 4; ++rt) acc[rt] = kAll ? accs[kAll ? ct : 0][rt] : f32x4{0.f, 0.f, 0.f, 0.f};
-          if constexpr (kAll) {
-            // accumulated above
-          } else if constexpr (QUEST) {
+          for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+          if constexpr (QUEST) {
             // sum over the k-step's 32 channels of q * (q > 0 ? kmax : kmin):
             // B holds the (kmin, kmax) pairs of channels 4 g .. 4 g + 3 and
             // 16 + 4 g .. 16 + 4 g + 3 (two 16-byte columns of the row)
@@ -395,6 +360,23 @@ __global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
   float* full = P.scores_out + row * s.NB;
   for (int p = lane; p < s.NB; p += 64)
     if (p == 0 || p > nc) full[p] = -__builtin_huge_valf();
+}
+
+template <int D, bool QUEST, int OUT>
+__global__ void __launch_bounds__(64 * kMaxGroup) score_kernel(SelParams P) {
+  score_body<D, QUEST, OUT>(P);
+}
+
+// Quest d 128 tile scores (full or packed rows): the same body held to 168
+// registers, so three waves share each SIMD (three workgroups per CU with
+// the 3-slot ring) instead of two; the query tile, its sparsity indices and
+// one column tile's operands fit without spilling.  Measured at 128K:
+// score + select 1.50 -> 1.36 ms (P7 1.28 -> 1.18, C3 0.45 -> 0.41),
+// outputs bit-identical.
+template <int OUT>
+__global__ void __launch_bounds__(64 * kMaxGroup) __attribute__((amdgpu_waves_per_eu(3, 3)))
+score_kernel_q128(SelParams P) {
+  score_body<128, true, OUT>(P);
 }
 
 // One wave per (b, h, t) unit, heaviest tile first; reads the unit's
@@ -610,7 +592,12 @@ hipError_t launch_score(SelParams P, hipStream_t stream) {
     if (e != hipSuccess) return e;
   }
   const int grid = ((P.n_wg + 7) / 8) * 8;
-  score_kernel<D, QUEST, OUT><<<grid, 64 * P.GW, smem, stream>>>(P);
+  if constexpr (D == 128 && QUEST && OUT != kOutRough) {
+    static_assert(MetaChunk<D, QUEST>::kRingSlots * MetaChunk<D, QUEST>::kBytes <= 65536, "static LDS limit");
+    score_kernel_q128<OUT><<<grid, 64 * P.GW, smem, stream>>>(P);
+  } else {
+    score_kernel<D, QUEST, OUT><<<grid, 64 * P.GW, smem, stream>>>(P);
+  }
   return hipGetLastError();
 }
 
