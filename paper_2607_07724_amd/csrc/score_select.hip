@@ -379,6 +379,17 @@ score_kernel_q128(SelParams P) {
   score_body<128, true, OUT>(P);
 }
 
+// K-mean d 128 tile scores: the body held to 96 registers, five waves per
+// SIMD instead of four (the 16 KiB ring allows it; a few values spill to
+// scratch): score + select 1.09 -> 0.99 ms on the 28/4-head d 128 layer at
+// 128K, outputs bit-identical.  (K-mean d 256 held to three waves spills
+// 65 registers and runs 1.5x slower; it keeps two.)
+template <int OUT>
+__global__ void __launch_bounds__(64 * kMaxGroup) __attribute__((amdgpu_waves_per_eu(5, 5)))
+score_kernel_k128(SelParams P) {
+  score_body<128, false, OUT>(P);
+}
+
 // One wave per (b, h, t) unit, heaviest tile first; reads the unit's
 // candidate scores (packed rows of the score kernel, or a full [.., N_B] row)
 // SLOTS: candidates per lane held in registers (N_B / 64 rounded up to 32 or
@@ -595,6 +606,8 @@ hipError_t launch_score(SelParams P, hipStream_t stream) {
   if constexpr (D == 128 && QUEST && OUT != kOutRough) {
     static_assert(MetaChunk<D, QUEST>::kRingSlots * MetaChunk<D, QUEST>::kBytes <= 65536, "static LDS limit");
     score_kernel_q128<OUT><<<grid, 64 * P.GW, smem, stream>>>(P);
+  } else if constexpr (D == 128 && !QUEST && OUT != kOutRough) {
+    score_kernel_k128<OUT><<<grid, 64 * P.GW, smem, stream>>>(P);
   } else {
     score_kernel<D, QUEST, OUT><<<grid, 64 * P.GW, smem, stream>>>(P);
   }
