@@ -26,6 +26,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "routed block-sparse prefill ms + TFLOP/s vs dense at 32K-128K, 1 MI355X"
 PEAK_BF16_TFLOPS = 2500.0
+# the 2:4-sparse bf16 instruction the Quest scoring runs on, dense-equivalent FLOP
+PEAK_BF16_SPARSE_TFLOPS = 5000.0
 PEAK_HBM_GBS = 8000.0
 
 
@@ -151,14 +153,18 @@ def stage_roofline(w, stage_ms, f_sc, f_att, n_trig):
         gbs = by / (ms * 1e-3) / 1e9
         return {"bytes": int(by), "GBps": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
 
-    def mfma(fl, ms):
+    def mfma(fl, ms, peak=PEAK_BF16_TFLOPS):
         tf = fl / (ms * 1e-3) / 1e12
-        return {"flop": fl, "TFLOPs": round(tf, 2), "frac_mfma": round(tf / PEAK_BF16_TFLOPS, 4)}
+        return {"flop": fl, "TFLOPs": round(tf, 2), "mfma_peak_TFLOPs": peak, "frac_mfma": round(tf / peak, 4)}
+
+    # Quest scores run on the 2:4-sparse instruction (twice the dense rate);
+    # its FLOP are counted dense-equivalent, so they are held to that peak
+    score_peak = PEAK_BF16_SPARSE_TFLOPS if w.backbone == 1 else PEAK_BF16_TFLOPS
 
     return {
         "block_meta": {"ms": round(float(stage_ms[0]), 4), "bound": "hbm", **hbm(meta_b, stage_ms[0])},
         "score_select": {"ms": round(float(stage_ms[1]), 4), "bound": "mfma",
-                         **mfma(f_sc, stage_ms[1]), **hbm(score_b, stage_ms[1])},
+                         **mfma(f_sc, stage_ms[1], score_peak), **hbm(score_b, stage_ms[1])},
         "route": {"ms": round(float(stage_ms[2]), 4), "bound": "hbm (launch latency)",
                   **hbm(route_b, stage_ms[2])},
         "attend": {"ms": round(float(stage_ms[3]), 4), "bound": "mfma", **mfma(f_att, stage_ms[3])},

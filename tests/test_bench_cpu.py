@@ -130,3 +130,15 @@ def test_cpu_leg_parity_on_oracle_outputs():
         bad[b, h, t, len(row) - 1] = spare[-1]
         r2 = bench.cpu_baseline(w, inp, units, bad, trig.astype(np.uint8), O_units, threads=2)
         assert r2["parity"]["kv_rows_beyond_near_ties"] >= 1 and not r2["parity"]["ok"]
+
+
+def test_stage_roofline_holds_quest_scoring_to_the_sparse_peak():
+    """The Quest score contraction runs on the 2:4-sparse instruction, so its
+    dense-equivalent FLOP are held to the 5.0 PFLOP/s sparse peak; K-mean
+    and the attention to the 2.5 PFLOP/s dense one."""
+    for backbone, peak in ((synth.QUEST, 5000.0), (synth.KMEAN, 2500.0)):
+        w = synth.WORKLOADS["C2"].replace(backbone=backbone)
+        st = bench.stage_roofline(w, [1.0, 1.0, 1.0, 1.0], 2.5e12, 2.5e12, 10)
+        assert st["score_select"]["mfma_peak_TFLOPs"] == peak
+        assert st["score_select"]["frac_mfma"] == round(2500.0 / peak, 4)
+        assert st["attend"]["mfma_peak_TFLOPs"] == 2500.0 and st["attend"]["frac_mfma"] == 1.0
