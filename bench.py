@@ -462,8 +462,9 @@ def main():
         log(f"measured peaks: {probe}")
         roofline["measured_peak_TFLOPs"] = probe["gemm_bf16_TFLOPs"]
         roofline["frac_of_measured_peak"] = round(roofline["achieved"] / probe["gemm_bf16_TFLOPs"], 4)
-        roofline["mfma_loop_TFLOPs"] = probe["mfma_loop_bf16_TFLOPs"]
-        roofline["frac_of_mfma_loop"] = round(roofline["achieved"] / probe["mfma_loop_bf16_TFLOPs"], 4)
+        if probe["mfma_loop_bf16_TFLOPs"]:
+            roofline["mfma_loop_TFLOPs"] = probe["mfma_loop_bf16_TFLOPs"]
+            roofline["frac_of_mfma_loop"] = round(roofline["achieved"] / probe["mfma_loop_bf16_TFLOPs"], 4)
 
     # GPU outputs of the units the CPU leg samples, copied before the big legs free memory
     cpu = None
@@ -872,6 +873,9 @@ def mfma_loop_peaks(torch, dev, stream, n_wg=2048, iters=4000, reps=5):
     tight loop of dense and of 2:4-sparse bf16 matrix instructions."""
     import ctypes
     from paper_2607_07724_amd import build
+    if not os.path.exists(build.PROBE_LIB):
+        log(f"{build.PROBE_LIB} is not built: no matrix-core loop ceilings")
+        return {"mfma_loop_bf16_TFLOPs": None, "smfmac_loop_bf16_TFLOPs": None}
     L = ctypes.CDLL(build.PROBE_LIB)
     L.ugbs_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
     L.ugbs_probe_flop.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
