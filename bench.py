@@ -861,11 +861,54 @@ def measured_peaks(torch, dev, stream):
     gemm = 10 * 2.0 * n ** 3 / (e0.elapsed_time(e1) * 1e-3) / 1e12
     del A, B, C
     loops = mfma_loop_peaks(torch, dev, stream)
-    return {"copy_GBps": round(copy_gbps, 1), "gemm_bf16_TFLOPs": round(gemm, 1), **loops,
+    fill = lds_fill_rates(torch, dev, stream)
+    return {"copy_GBps": round(copy_gbps, 1), "gemm_bf16_TFLOPs": round(gemm, 1), **loops, "lds_fill": fill,
             "copy": "torch elementwise add, 1 GiB in + 1 GiB out", "gemm": "torch.matmul bf16 8192^3",
             "mfma_loop": "libugbs_probe: 2048 workgroups x 4 waves, back-to-back 16x16x32 bf16 MFMA "
                          "(dense) or 16x16x64 bf16 2:4-sparse MFMA (dense-equivalent FLOP) on 8 "
                          "accumulator chains per wave, operands toggling every iteration"}
+
+
+def lds_fill_rates(torch, dev, stream, iters=800):
+    """The attention kernel's staging path on its own: 16 KiB tiles chosen at
+    random from a region that fits one XCD's L2 (2 MiB), the memory-side
+    cache (64 MiB) or neither (2 GiB), streamed into LDS by direct loads,
+    four 2-wave workgroups per CU with two tiles in flight each.  Bytes per
+    second, and per clock and CU at the clock the kernel ran at."""
+    import ctypes
+    from paper_2607_07724_amd import build
+    if not os.path.exists(build.PROBE_LIB):
+        return None
+    L = ctypes.CDLL(build.PROBE_LIB)
+    L.ugbs_probe_fill.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_uint, ctypes.c_int, ctypes.c_int,
+                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    L.ugbs_probe_out_floats.argtypes = [ctypes.c_int]
+    n_cu = torch.cuda.get_device_properties(dev).multi_processor_count
+    n_wg = 4 * n_cu
+    src = torch.ones(1 << 30, dtype=torch.int16, device=dev)      # 2 GiB
+    clk = torch.zeros(2, dtype=torch.int64, device=dev)
+    out = torch.empty(L.ugbs_probe_out_floats(n_wg), dtype=torch.float32, device=dev)
+    st = ctypes.c_void_p(stream.cuda_stream)
+    res = {}
+    for name, mib in (("l2_resident_2MiB", 2), ("memory_side_cache_64MiB", 64), ("hbm_2GiB", 2048)):
+        args = (2, ctypes.c_void_p(src.data_ptr()), mib * 64, n_wg, iters, ctypes.c_void_p(clk.data_ptr()),
+                ctypes.c_void_p(out.data_ptr()), st)
+        assert L.ugbs_probe_fill(*args) == 0
+        torch.cuda.synchronize(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        assert L.ugbs_probe_fill(*args) == 0
+        e1.record(stream)
+        torch.cuda.synchronize(dev)
+        sec = e0.elapsed_time(e1) * 1e-3
+        ticks, real = clk.cpu().tolist()
+        ghz = ticks / (real / 100e6) / 1e9 if real > 0 else None
+        by = n_wg * iters * 16384
+        res[name] = {"TBps": round(by / sec / 1e12, 2), "clock_GHz": round(ghz, 2) if ghz else None,
+                     "bytes_per_clk_per_cu": round(by / sec / n_cu / (ghz * 1e9), 1) if ghz else None}
+    del src, out
+    res["pattern"] = "16 KiB tiles, random per workgroup, direct-to-LDS, 4 x 2-wave workgroups per CU, 2 tiles in flight"
+    return res
 
 
 def mfma_loop_peaks(torch, dev, stream, n_wg=2048, iters=4000, reps=5):

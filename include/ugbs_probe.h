@@ -1,6 +1,6 @@
 /*
- * ugbs_probe.h -- matrix-core ceilings of the device, measured by a tight
- * loop of matrix instructions (libugbs_probe.so).  Measurement support for
+ * ugbs_probe.h -- matrix-core and LDS-fill ceilings of the device, measured
+ * by tight loops (libugbs_probe.so).  Measurement support for
  * the benchmark's roofline context; not part of the method's path.
  */
 #ifndef UGBS_PROBE_H
@@ -29,8 +29,20 @@ UGBS_PROBE_API int ugbs_probe_mfma(int kind, int n_workgroups, int iters, float*
 /* Dense-equivalent FLOP of one ugbs_probe_mfma call with these arguments. */
 UGBS_PROBE_API double ugbs_probe_flop(int kind, int n_workgroups, int iters);
 
-/* Floats written to `out` by ugbs_probe_mfma. */
+/* Floats written to `out` by ugbs_probe_mfma and ugbs_probe_fill. */
 UGBS_PROBE_API int ugbs_probe_out_floats(int n_workgroups);
+
+/* Fill rate of the attention kernel's staging path: n_workgroups
+ * workgroups of 128 threads each stream `iters` 16 KiB tiles, chosen at
+ * random among the n_tiles tiles of `src` (device memory of n_tiles * 16
+ * KiB, caller-owned), into LDS with direct loads, at most `depth` (1 or 2)
+ * tiles in flight per workgroup.  clk (device, 2 x uint64) receives the
+ * shader-clock and the 100 MHz constant-clock ticks of workgroup 0's run;
+ * out (device, ugbs_probe_out_floats(n_workgroups) floats) keeps the LDS
+ * contents live.  Returns 0, 1 for invalid arguments (nothing enqueued), 2
+ * for a failed launch. */
+UGBS_PROBE_API int ugbs_probe_fill(int depth, const void* src, unsigned n_tiles, int n_workgroups,
+                                   int iters, unsigned long long* clk, float* out, void* stream);
 
 #ifdef __cplusplus
 }

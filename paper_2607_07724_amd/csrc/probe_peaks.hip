@@ -1,5 +1,6 @@
-// Matrix-core ceilings of the device this runs on, for the benchmark's
-// roofline context (libugbs_probe.so; not part of the method's path).
+// Matrix-core and LDS-fill ceilings of the device this runs on, for the
+// benchmark's roofline context (libugbs_probe.so; not part of the method's
+// path).
 //
 // Each wave issues back-to-back matrix instructions on eight independent
 // accumulator chains (enough to keep the pipeline full at two or more waves
@@ -94,9 +95,70 @@ __global__ void __launch_bounds__(kThreads) mfma_loop(float* out, int iters) {
   out[tid] = s;
 }
 
+// Fill rate of 16 KiB tiles from a source region into LDS by direct loads
+// (global_load_lds_dwordx4), the attention kernel's staging path: each
+// workgroup of 128 threads (two waves, as the attention units) streams
+// tiles chosen by a per-workgroup random sequence over the region, each
+// wave issuing eight 1 KiB loads per tile, with up to two tiles in flight
+// (two 16 KiB LDS slots, so four workgroups fit a CU as the attention's
+// units do).  One lane of workgroup 0 records the shader-clock and
+// constant-clock counters over its run, from which the host derives the
+// clock.  Every load stays inside tile (h mod n_tiles) of the region.
+__device__ __forceinline__ void fill_dma16(const uint16_t* base, uint32_t voff, uint32_t lds_byte_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(base), "s"(lds_byte_addr)
+               : "memory");
+}
+
+template <int DEPTH>
+__global__ void __launch_bounds__(128) fill_loop(const uint16_t* src, uint32_t n_tiles, int iters,
+                                                 unsigned long long* clk, float* out) {
+  __shared__ __align__(16) uint16_t s_buf[2 * 8192];   // two 16 KiB tiles
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)s_buf;
+  unsigned long long t0 = 0, r0 = 0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    t0 = __builtin_amdgcn_s_memtime();
+    r0 = __builtin_amdgcn_s_memrealtime();
+  }
+  uint32_t h = blockIdx.x * 2654435761u;
+  for (int i = 0; i < iters; ++i) {
+    h = h * 1664525u + 1013904223u;
+    const uint16_t* base = src + (size_t)(h % n_tiles) * 8192 + (size_t)w * 4096;   // this wave's 8 KiB
+    const uint32_t slot = lds0 + (uint32_t)((i % 2) * 16384 + w * 8192);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      fill_dma16(base + j * 512, (uint32_t)(lane * 16), __builtin_amdgcn_readfirstlane(slot + j * 1024));
+    // at most DEPTH - 1 tiles of this wave still in flight (loads complete in issue order)
+    __builtin_amdgcn_s_waitcnt(DEPTH == 1 ? 0x0f70 : 0x0f78);
+  }
+  __builtin_amdgcn_s_waitcnt(0x0f70);
+  __syncthreads();
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    clk[0] = __builtin_amdgcn_s_memtime() - t0;
+    clk[1] = __builtin_amdgcn_s_memrealtime() - r0;
+  }
+  out[blockIdx.x * 128 + threadIdx.x] = (float)s_buf[threadIdx.x];
+}
+
 }  // namespace
 
 extern "C" {
+
+int ugbs_probe_fill(int depth, const void* src, unsigned n_tiles, int n_workgroups, int iters,
+                    unsigned long long* clk, float* out, void* stream) {
+  if ((depth != 1 && depth != 2) || !src || !clk || !out || n_tiles < 1 || n_workgroups < 1 || iters < 1)
+    return 1;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const uint16_t* p = static_cast<const uint16_t*>(src);
+  if (depth == 1)
+    fill_loop<1><<<n_workgroups, 128, 0, s>>>(p, n_tiles, iters, clk, out);
+  else
+    fill_loop<2><<<n_workgroups, 128, 0, s>>>(p, n_tiles, iters, clk, out);
+  return hipGetLastError() == hipSuccess ? 0 : 2;
+}
 
 int ugbs_probe_mfma(int kind, int n_workgroups, int iters, float* out, void* stream) {
   if (n_workgroups < 1 || iters < 1 || !out || (kind != UGBS_PROBE_MFMA_BF16 && kind != UGBS_PROBE_SMFMAC_BF16))

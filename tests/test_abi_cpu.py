@@ -395,7 +395,7 @@ def test_probe_library_exports_and_rejects_bad_arguments():
         pytest.skip("probe library not built here (run __graft_entry__.build())")
     txt = open(os.path.join(ROOT, "include", "ugbs_probe.h")).read()
     names = sorted(set(re.findall(r"UGBS_PROBE_API\s+[\w\s\*]+?\b(ugbs_\w+)\s*\(", txt)))
-    assert names == ["ugbs_probe_flop", "ugbs_probe_mfma", "ugbs_probe_out_floats"]
+    assert names == ["ugbs_probe_fill", "ugbs_probe_flop", "ugbs_probe_mfma", "ugbs_probe_out_floats"]
     L = ctypes.CDLL(build.PROBE_LIB)
     for n in names:
         assert hasattr(L, n), n
@@ -410,3 +410,10 @@ def test_probe_library_exports_and_rejects_bad_arguments():
     assert L.ugbs_probe_flop(0, 3, 5) == 16 * 16 * 32 * 2 * 16 * 5 * 3 * 4
     assert L.ugbs_probe_flop(1, 3, 5) == 2 * L.ugbs_probe_flop(0, 3, 5)
     assert L.ugbs_probe_out_floats(3) == 3 * 256
+    L.ugbs_probe_fill.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_uint, ctypes.c_int, ctypes.c_int,
+                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    assert L.ugbs_probe_fill(3, fake, 8, 8, 8, fake, fake, None) == 1
+    assert L.ugbs_probe_fill(2, None, 8, 8, 8, fake, fake, None) == 1
+    assert L.ugbs_probe_fill(2, fake, 0, 8, 8, fake, fake, None) == 1
+    assert L.ugbs_probe_fill(1, fake, 8, 8, 0, fake, fake, None) == 1
+    assert L.ugbs_probe_fill(1, fake, 8, 8, 8, None, fake, None) == 1
