@@ -17,9 +17,11 @@
 // rows (the B operand) come in chunks of 16 or 32 blocks that the workgroup's
 // waves fetch together with direct-to-LDS loads into a ring of 3 or 4 slots
 // (two or three chunks in flight), so each chunk crosses L2 once per
-// workgroup; in LDS
-// the 16-byte column c of row r sits at c ^ (r mod 16), which makes the
-// operand reads bank-conflict free.  The max over the tile's rows (A.3) is
+// workgroup; in LDS the 16-byte column c of row r sits at c ^ (r mod 16),
+// which makes the operand reads bank-conflict free.  Occupancy decides the
+// speed: Quest d 128 and K-mean d 128 launch the same body through entries
+// held to fewer registers (three and five waves per SIMD, see
+// score_kernel_q128 / score_kernel_k128).  The max over the tile's rows (A.3) is
 // the max over a lane's 16 accumulators and then across the four 16-lane
 // groups; each chunk's 16 tile scores go straight to memory, into the
 // caller's [.., N_B] score tensor or into packed rows of the workspace (row
@@ -35,9 +37,10 @@
 // index) and ordered by (key, ~index) with a bitonic sort: in registers
 // across lanes for R <= 128, in LDS above.  sigma uses IEEE fp32 subtract and
 // divide.  The kernel is bound by instruction issue, not by its reads: on
-// the 128K layer about 1600 VALU instructions per unit keep the VALU active
-// for ~87% of the SIMD cycles.  Splitting the stages keeps each kernel at its own occupancy (the
-// scoring kernel is bound by registers, the selection kernel by latency).
+// the 128K layer about 1,620 VALU instructions per unit keep the SIMDs'
+// VALU issue ~84% busy.  Splitting the stages keeps each kernel at its own
+// occupancy (the scoring kernel is bound by registers, the selection
+// kernel by instruction issue).
 #include "select_common.h"
 
 namespace ugbs {
