@@ -38,8 +38,8 @@ UGBS_PROBE_API int ugbs_probe_out_floats(int n_workgroups);
  * KiB, caller-owned), into LDS with direct loads, at most `depth` (1 or 2)
  * tiles in flight per workgroup.  clk (device, 2 x uint64) receives the
  * shader-clock and the 100 MHz constant-clock ticks of workgroup 0's run;
- * out (device, ugbs_probe_out_floats(n_workgroups) floats) keeps the LDS
- * contents live.  Returns 0, 1 for invalid arguments (nothing enqueued), 2
+ * out (device, ugbs_probe_out_floats(n_workgroups) floats; the first 128
+ * per workgroup are written) keeps the LDS contents live.  Returns 0, 1 for invalid arguments (nothing enqueued), 2
  * for a failed launch. */
 UGBS_PROBE_API int ugbs_probe_fill(int depth, const void* src, unsigned n_tiles, int n_workgroups,
                                    int iters, unsigned long long* clk, float* out, void* stream);
