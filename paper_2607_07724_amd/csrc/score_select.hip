@@ -21,7 +21,9 @@
 // which makes the operand reads bank-conflict free.  Occupancy decides the
 // speed: Quest d 128 and K-mean d 128 launch the same body through entries
 // held to fewer registers (three and five waves per SIMD, see
-// score_kernel_q128 / score_kernel_k128).  The max over the tile's rows (A.3) is
+// score_kernel_q128 / score_kernel_k128).  Where registers allow (Quest d <=
+// 128, K-mean d 256) a column tile's B operands are all read before its
+// first matrix instruction, so each column tile waits on the LDS once.  The max over the tile's rows (A.3) is
 // the max over a lane's 16 accumulators and then across the four 16-lane
 // groups; each chunk's 16 tile scores go straight to memory, into the
 // caller's [.., N_B] score tensor or into packed rows of the workspace (row
@@ -285,7 +287,7 @@ __device__ __forceinline__ void score_body(const SelParams& P) {
         }
         return;
       }
-#pragma unroll
+#pragma unroll 1
       for (int j = 0; j < kMaxMine; ++j) {
         const int i = w + j * P.GW;
         if (i < MC::kLoads) dma16(base, lane_off(i, c, last), __builtin_amdgcn_readfirstlane(slot + i * 1024));
@@ -295,7 +297,14 @@ __device__ __forceinline__ void score_body(const SelParams& P) {
 
     for (int c = 0; c < nchunks; ++c) {
       const int after = min(MC::kRingSlots - 2, nchunks - 1 - c);  // chunks issued after c
-      wait_vmcnt_dyn(n_mine * after);
+      if (fast) {
+        // each wave issues kMine loads per chunk: one uniform branch
+        if (after <= 0) wait_vm<0>();
+        else if (after == 1) wait_vm<kMine>();
+        else wait_vmcnt_dyn(kMine * after);
+      } else {
+        wait_vmcnt_dyn(n_mine * after);
+      }
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of chunk c-1 are done
       lds_barrier();                                    // chunk c landed; chunk c-1 is free
       if (c + MC::kRingSlots - 1 < nchunks) issue(c + MC::kRingSlots - 1);
@@ -311,22 +320,60 @@ __device__ __forceinline__ void score_body(const SelParams& P) {
             // sum over the k-step's 32 channels of q * (q > 0 ? kmax : kmin):
             // B holds the (kmin, kmax) pairs of channels 4 g .. 4 g + 3 and
             // 16 + 4 g .. 16 + 4 g + 3 (two 16-byte columns of the row)
+            if constexpr (KA <= 4) {
+              // d <= 128: all of the column tile's B operands are read
+              // first, so the LDS latency is paid once per column tile
+              // instead of once per k-step
+              uint4 bb[KA][2];
 #pragma unroll
-            for (int ks = 0; ks < KA; ++ks) {
-              const uint4 b0 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + g));
-              const uint4 b1 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + 4 + g));
-              const bf16x16 b = as_bf16x16(b0, b1);
+              for (int ks = 0; ks < KA; ++ks) {
+                bb[ks][0] = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + g));
+                bb[ks][1] = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + 4 + g));
+              }
 #pragma unroll
-              for (int rt = 0; rt < 4; ++rt)
-                acc[rt] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[rt][ks], b, acc[rt], (int)qidx[rt][ks], 0, 0);
+              for (int ks = 0; ks < KA; ++ks) {
+                const bf16x16 b = as_bf16x16(bb[ks][0], bb[ks][1]);
+#pragma unroll
+                for (int rt = 0; rt < 4; ++rt)
+                  acc[rt] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[rt][ks], b, acc[rt], (int)qidx[rt][ks], 0, 0);
+              }
+              __builtin_amdgcn_sched_group_barrier(0x100, 2 * KA, 0);
+              __builtin_amdgcn_sched_group_barrier(0x008, 4 * KA, 0);
+            } else {
+#pragma unroll
+              for (int ks = 0; ks < KA; ++ks) {
+                const uint4 b0 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + g));
+                const uint4 b1 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + 4 + g));
+                const bf16x16 b = as_bf16x16(b0, b1);
+#pragma unroll
+                for (int rt = 0; rt < 4; ++rt)
+                  acc[rt] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[rt][ks], b, acc[rt], (int)qidx[rt][ks], 0, 0);
+              }
             }
           } else {
+            if constexpr (D == 256) {
+              // the column tile's B operands are read first (as above); at
+              // d 128 the five-wave entry has no registers for them
+              uint4 bb[KS];
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-              const bf16x8 b = as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(br, 4 * ks + g)));
+              for (int ks = 0; ks < KS; ++ks) bb[ks] = *reinterpret_cast<const uint4*>(slot + MC::off(br, 4 * ks + g));
 #pragma unroll
-              for (int rt = 0; rt < 4; ++rt)
-                acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][ks], b, acc[rt], 0, 0, 0);
+              for (int ks = 0; ks < KS; ++ks) {
+                const bf16x8 b = as_bf16x8(bb[ks]);
+#pragma unroll
+                for (int rt = 0; rt < 4; ++rt)
+                  acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][ks], b, acc[rt], 0, 0, 0);
+              }
+              __builtin_amdgcn_sched_group_barrier(0x100, KS, 0);
+              __builtin_amdgcn_sched_group_barrier(0x008, 4 * KS, 0);
+            } else {
+#pragma unroll
+              for (int ks = 0; ks < KS; ++ks) {
+                const bf16x8 b = as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(br, 4 * ks + g)));
+#pragma unroll
+                for (int rt = 0; rt < 4; ++rt)
+                  acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][ks], b, acc[rt], 0, 0, 0);
+              }
             }
           }
           const int pos = MC::kBlocks * c + br;
