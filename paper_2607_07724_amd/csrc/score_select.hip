@@ -23,7 +23,8 @@
 // held to fewer registers (three and five waves per SIMD, see
 // score_kernel_q128 / score_kernel_k128).  Where registers allow (Quest d <=
 // 128, K-mean d 256) a column tile's B operands are all read before its
-// first matrix instruction, so each column tile waits on the LDS once.  The max over the tile's rows (A.3) is
+// first matrix instruction, so each column tile waits on the LDS once, and
+// the next column tile's reads go out before this tile's max and store.  The max over the tile's rows (A.3) is
 // the max over a lane's 16 accumulators and then across the four 16-lane
 // groups; each chunk's 16 tile scores go straight to memory, into the
 // caller's [.., N_B] score tensor or into packed rows of the workspace (row
@@ -310,70 +311,80 @@ __device__ __forceinline__ void score_body(const SelParams& P) {
       if (c + MC::kRingSlots - 1 < nchunks) issue(c + MC::kRingSlots - 1);
       if (active) {
         const unsigned char* slot = ring + (c % MC::kRingSlots) * MC::kBytes;
+        constexpr int NCT = MC::kBlocks / 16;            // 16-block column tiles per chunk
+        // Read-ahead form (Quest d <= 128, K-mean d 256; elsewhere the
+        // registers are not there): all B operands of a column tile are read
+        // before its first matrix instruction, so the tile waits on the LDS
+        // once, and the next column tile's reads are issued right after this
+        // tile's matrix instructions, ahead of its max and store.  Quest: B
+        // holds the (kmin, kmax) pairs of channels 4 g .. 4 g + 3 and 16 + 4 g
+        // .. 16 + 4 g + 3 of each 32-channel k-step (two 16-byte columns).
+        constexpr bool AHEAD = QUEST ? (KA <= 4) : (D == 256);
+        constexpr int NRD = QUEST ? 2 * KA : KS;          // 16-byte operand reads per column tile
+        uint4 bb[AHEAD ? NRD : 1];
+        auto read_b = [&](int ct) {
+          const int br = 16 * ct + c16;
 #pragma unroll
-        for (int ct = 0; ct < MC::kBlocks / 16; ++ct) {   // 16-block column tiles of the chunk
+          for (int j = 0; j < NRD; ++j) {
+            const int col = QUEST ? 8 * (j >> 1) + 4 * (j & 1) + g : 4 * j + g;
+            bb[j] = *reinterpret_cast<const uint4*>(slot + MC::off(br, col));
+          }
+        };
+        // the roughness mode keeps its registers for the row differences and
+        // reads each column tile's operands at the tile's start
+        constexpr bool EARLY = AHEAD && !ROUGH;
+        if constexpr (AHEAD) {
+          read_b(0);
+          __builtin_amdgcn_sched_barrier(0);   // keep the reads ahead of the matrix instructions
+        }
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) {
           const int br = 16 * ct + c16;                  // block row of this lane's column
+          if constexpr (AHEAD && !EARLY) {
+            if (ct > 0) read_b(ct);
+            __builtin_amdgcn_sched_barrier(0);
+          }
           f32x4 acc[4];
 #pragma unroll
           for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if constexpr (QUEST) {
-            // sum over the k-step's 32 channels of q * (q > 0 ? kmax : kmin):
-            // B holds the (kmin, kmax) pairs of channels 4 g .. 4 g + 3 and
-            // 16 + 4 g .. 16 + 4 g + 3 (two 16-byte columns of the row)
-            if constexpr (KA <= 4) {
-              // d <= 128: all of the column tile's B operands are read
-              // first, so the LDS latency is paid once per column tile
-              // instead of once per k-step
-              uint4 bb[KA][2];
+          if constexpr (AHEAD) {
 #pragma unroll
-              for (int ks = 0; ks < KA; ++ks) {
-                bb[ks][0] = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + g));
-                bb[ks][1] = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + 4 + g));
-              }
-#pragma unroll
-              for (int ks = 0; ks < KA; ++ks) {
-                const bf16x16 b = as_bf16x16(bb[ks][0], bb[ks][1]);
+            for (int ks = 0; ks < KS / (QUEST ? 2 : 1); ++ks) {
+              if constexpr (QUEST) {
+                const bf16x16 b = as_bf16x16(bb[2 * ks], bb[2 * ks + 1]);
 #pragma unroll
                 for (int rt = 0; rt < 4; ++rt)
                   acc[rt] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[rt][ks], b, acc[rt], (int)qidx[rt][ks], 0, 0);
-              }
-              __builtin_amdgcn_sched_group_barrier(0x100, 2 * KA, 0);
-              __builtin_amdgcn_sched_group_barrier(0x008, 4 * KA, 0);
-            } else {
-#pragma unroll
-              for (int ks = 0; ks < KA; ++ks) {
-                const uint4 b0 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + g));
-                const uint4 b1 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + 4 + g));
-                const bf16x16 b = as_bf16x16(b0, b1);
-#pragma unroll
-                for (int rt = 0; rt < 4; ++rt)
-                  acc[rt] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[rt][ks], b, acc[rt], (int)qidx[rt][ks], 0, 0);
-              }
-            }
-          } else {
-            if constexpr (D == 256) {
-              // the column tile's B operands are read first (as above); at
-              // d 128 the five-wave entry has no registers for them
-              uint4 bb[KS];
-#pragma unroll
-              for (int ks = 0; ks < KS; ++ks) bb[ks] = *reinterpret_cast<const uint4*>(slot + MC::off(br, 4 * ks + g));
-#pragma unroll
-              for (int ks = 0; ks < KS; ++ks) {
+              } else {
                 const bf16x8 b = as_bf16x8(bb[ks]);
 #pragma unroll
                 for (int rt = 0; rt < 4; ++rt)
                   acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][ks], b, acc[rt], 0, 0, 0);
               }
-              __builtin_amdgcn_sched_group_barrier(0x100, KS, 0);
-              __builtin_amdgcn_sched_group_barrier(0x008, 4 * KS, 0);
-            } else {
+            }
+            if constexpr (EARLY) {
+              __builtin_amdgcn_sched_barrier(0);
+              if (ct + 1 < NCT) read_b(ct + 1);
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          } else if constexpr (QUEST) {
+            // sum over the k-step's 32 channels of q * (q > 0 ? kmax : kmin)
 #pragma unroll
-              for (int ks = 0; ks < KS; ++ks) {
-                const bf16x8 b = as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(br, 4 * ks + g)));
+            for (int ks = 0; ks < KA; ++ks) {
+              const uint4 b0 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + g));
+              const uint4 b1 = *reinterpret_cast<const uint4*>(slot + MC::off(br, 8 * ks + 4 + g));
+              const bf16x16 b = as_bf16x16(b0, b1);
 #pragma unroll
-                for (int rt = 0; rt < 4; ++rt)
-                  acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][ks], b, acc[rt], 0, 0, 0);
-              }
+              for (int rt = 0; rt < 4; ++rt)
+                acc[rt] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(a[rt][ks], b, acc[rt], (int)qidx[rt][ks], 0, 0);
+            }
+          } else {
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+              const bf16x8 b = as_bf16x8(*reinterpret_cast<const uint4*>(slot + MC::off(br, 4 * ks + g)));
+#pragma unroll
+              for (int rt = 0; rt < 4; ++rt)
+                acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][ks], b, acc[rt], 0, 0, 0);
             }
           }
           const int pos = MC::kBlocks * c + br;
