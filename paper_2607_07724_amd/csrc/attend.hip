@@ -153,6 +153,85 @@ attend_kernel(AttnParams P) {
   const int j_xcd = blockIdx.x >> 3;
   const int period = (MODE == kBitmap ? 1 : 2) * P.conc;
   const int start_blk = (int)(((long long)(j_xcd % period) * u.t) / period);
+  // Selection modes, shared part: the unit's waves split the candidate
+  // loads, the keys, each lane's top-3 pre-filter and the survivor
+  // compaction (wave v takes the v-th contiguous slice of the slots, so the
+  // survivors land in position order, as one wave would write them); the
+  // exact threshold among the survivors stays with wave 0 below.  A lane's
+  // top 3 over the waves' slices is its top 3 over every slot, so the bound
+  // t0, the survivors and the kept set are those of the one-wave form.
+  int staged = -1;                                     // survivors staged in s_k, or -1
+  if constexpr (MODE == kSelect || MODE == kSelectWide) {
+    const int t = u.t;
+    const int nf = (t == 0) ? 1 : 2;
+    const int nc = (t >= 1) ? t - 1 : 0;
+    const int flag = __builtin_amdgcn_readfirstlane((int)P.sel_trigger[(size_t)u.b * s.T + t]);
+    const int R = min((flag != 0 ? s.W : s.k) - nf, nc);
+    if (R < nc && R <= 192) {
+      constexpr int NWV = Geo<D>::NWV;
+      constexpr int kSlots = MODE == kSelectWide ? UGBS_MAX_BLOCKS / 64 : 32;
+      static_assert(kSlots % NWV == 0, "slots split evenly over the waves");
+      constexpr int kPer = kSlots / NWV;
+      const int nslots = (nc + 63) / 64;
+      const float* src = P.sel_scores ? P.sel_scores + rowid * s.NB + 1
+                                      : P.sel_packed + packed_row(u.b * s.H + u.h, t, s.T);
+      uint32_t keys[kPer];
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        const int sl = w * kPer + j;
+        const int p = 64 * sl + lane;
+        keys[j] = (sl < nslots && p < nc) ? order_key(src[p]) : 0u;
+      }
+      uint32_t top3[3] = {0u, 0u, 0u};
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        const uint32_t x = keys[j];
+        top3[2] = max(top3[2], min(top3[1], x));
+        top3[1] = max(top3[1], min(top3[0], x));
+        top3[0] = max(top3[0], x);
+      }
+      uint32_t* s_t3 = reinterpret_cast<uint32_t*>(s_v);            // [NWV][3][64]
+      int* s_cnt = reinterpret_cast<int*>(s_t3 + NWV * 3 * 64);      // [NWV]
+#pragma unroll
+      for (int i = 0; i < 3; ++i) s_t3[(w * 3 + i) * 64 + lane] = top3[i];
+      __syncthreads();
+      uint32_t m3[3] = {0u, 0u, 0u};
+#pragma unroll
+      for (int v = 0; v < NWV * 3; ++v) {
+        const uint32_t x = s_t3[v * 64 + lane];
+        m3[2] = max(m3[2], min(m3[1], x));
+        m3[1] = max(m3[1], min(m3[0], x));
+        m3[0] = max(m3[0], x);
+      }
+      bool exact0;
+      const uint32_t t0 = kth_largest<3>(m3, 3, R, &exact0);
+      int mine = 0;
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) mine += __popcll(__ballot(t0 > 0u && keys[j] >= t0));
+      if (lane == 0) s_cnt[w] = mine;
+      __syncthreads();
+      int off = 0, ns = 0;
+#pragma unroll
+      for (int v = 0; v < NWV; ++v) {
+        const int c = s_cnt[v];
+        off += (v < w) ? c : 0;
+        ns += c;
+      }
+      constexpr int kSurv = 256;
+      if (t0 > 0u && ns <= kSurv) {
+        uint64_t* s_surv = reinterpret_cast<uint64_t*>(s_k);
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+          const bool tk = keys[j] >= t0;
+          const uint64_t mk = __ballot(tk);
+          if (tk) s_surv[off + lanes_below(mk)] = ((uint64_t)keys[j] << 32) | (uint32_t)(64 * (w * kPer + j) + lane);
+          off += __popcll(mk);
+        }
+        staged = ns;
+      }
+      __syncthreads();
+    }
+  }
   if (w == 0) {
     const int nwords = (u.t >> 5) + 1;                 // bitmap words covering blocks 0..t
     for (int i = lane; i < nwords; i += 64) s_bits[i] = 0u;
@@ -194,6 +273,22 @@ attend_kernel(AttnParams P) {
       }
       if (R >= nc) {
         for (int blk = 1 + lane; blk <= nc; blk += 64) atomicOr(&s_bits[blk >> 5], 1u << (blk & 31));
+      } else if (staged >= 0) {
+        // the survivors the waves staged: the exact R largest among them
+        constexpr int kSurv = 256;
+        const uint64_t* s_surv = reinterpret_cast<const uint64_t*>(s_k);
+        uint32_t k2[kSurv / 64], p2[kSurv / 64];
+#pragma unroll
+        for (int sl = 0; sl < kSurv / 64; ++sl) {
+          const int i = 64 * sl + lane;
+          const uint64_t v = (i < staged) ? s_surv[i] : 0ull;
+          k2[sl] = (uint32_t)(v >> 32);
+          p2[sl] = (uint32_t)v;
+        }
+        select_top_each<kSurv / 64>(k2, (staged + 63) / 64, R, lane, [&](int sl) {
+          const int blk = 1 + (int)p2[sl];
+          atomicOr(&s_bits[blk >> 5], 1u << (blk & 31));
+        });
       } else {
         const float* src = P.sel_scores ? P.sel_scores + rowid * s.NB + 1
                                         : P.sel_packed + packed_row(u.b * s.H + u.h, t, s.T);
