@@ -380,14 +380,17 @@ attend_kernel(AttnParams P) {
   // entries 0..n_rot-1 are visited from position rot0 on, cyclically
   const int n_rot = __builtin_amdgcn_readfirstlane(diag_last ? n - 1 : n);
   const int rot0 = __builtin_amdgcn_readfirstlane(s_below < n_rot ? s_below : 0);
-  auto listed = [&](int i) {
+  // listed_raw: the i-th block to visit as a per-lane LDS value (every lane
+  // the same); listed: the same, moved to a scalar register
+  auto listed_raw = [&](int i) {
     int p = i;
     if (i < n_rot) {
       p = i + rot0;
       if (p >= n_rot) p -= n_rot;
     }
-    return __builtin_amdgcn_readfirstlane(s_list[p]);
+    return s_list[p];
   };
+  auto listed = [&](int i) { return __builtin_amdgcn_readfirstlane(listed_raw(i)); };
 
   const size_t qo_base = ((size_t)u.b * s.H + u.h) * s.N + (size_t)u.t * kBlock;
   if (n == 0) {  // no attended key: O = 0
@@ -482,8 +485,14 @@ attend_kernel(AttnParams P) {
   compute_s(sc);
   wait_lgkm0();
   lds_barrier();                         // all waves are done reading s_k
+  // The indices of the next two blocks travel one step ahead: the LDS read
+  // of block it + 3 goes out at the end of step it, and its scalar copy is
+  // taken where step it + 1 needs it, so no list read waits on the LDS
+  // right after a barrier.
+  int nb1 = (n > 1) ? listed(1) : 0;     // block it + 1
+  int raw2 = (n > 2) ? listed_raw(2) : 0;  // block it + 2, per-lane copy
   if (n > 1) {
-    fetch_k(listed(1));
+    fetch_k(nb1);
     wait_vmcnt<0>();                     // K1 (and V0) landed
     lds_barrier();
   }
@@ -494,7 +503,7 @@ attend_kernel(AttnParams P) {
     constexpr bool MASK = decltype(mask_tag)::value;
     const bool has_next = it + 1 < n;
     const bool has_next2 = it + 2 < n;
-    const int nblk = has_next ? listed(it + 1) : 0;
+    const int nblk = has_next ? nb1 : 0;
 
     // S(it+1): on the last block this re-reads s_k (no fetch is pending) and is discarded
     f32x4 sn[4][RT];
@@ -568,7 +577,7 @@ attend_kernel(AttnParams P) {
     wait_lgkm0();
     wait_vmcnt<0>();
     lds_barrier();
-    if (has_next2) fetch_k(listed(it + 2));
+    if (has_next2) fetch_k(__builtin_amdgcn_readfirstlane(raw2));
 
     __builtin_amdgcn_s_setprio(1);
     if (__ballot(moved)) {
@@ -616,6 +625,8 @@ attend_kernel(AttnParams P) {
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) sc[kt][rt] = sn[kt][rt];
+    nb1 = __builtin_amdgcn_readfirstlane(raw2);
+    raw2 = (it + 3 < n) ? listed_raw(it + 3) : 0;
   };
 
   for (int it = 0; it + 1 < n; ++it) step(it, std::false_type{});
