@@ -571,6 +571,9 @@ attend_kernel(AttnParams P) {
       }
     }
 
+    // the whole softmax stays above the barrier, where it overlaps the
+    // landing of V(it)
+    __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_setprio(0);
     // one barrier: every wave is done reading s_k, and V(it), the only load
     // in flight, has landed
